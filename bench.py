@@ -1,0 +1,219 @@
+"""Benchmark of one mixed-batch serving step on one MI355X.
+
+A step is one pass of the hot path over one batch: the host batch former
+(token budget, cost, priority, greedy packing), the host planner, the
+upload of the work list, and the attention launch(es) over the paged cache;
+for workloads that move paused requests it also resumes and parks them.
+Inputs are synthetic, seeded, and resident in HBM before timing starts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode-8b]
+
+Prints one JSON line. ``value`` is query tokens per second of whole steps;
+``roofline`` relates the attention launches' algorithmic bytes (each KV byte
+a request reads counted once, plus Q, O and block ids) to their duration,
+measured with HIP events on the launch stream; ``cpu_baseline`` times the
+CPU oracle on a bounded sample of the same batch.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFS = 2516.6
+
+WORKLOADS = {
+    "tiny-mixed": 1,
+    "decode-8b": 2,
+    "mixed-8b": 3,
+    "long-context-8b": 4,
+}
+
+
+def algorithmic_bytes(b) -> float:
+    elem = {"f32": 4, "bf16": 2, "fp8": 1}
+    kv = float(np.sum(b.ctx_len.astype(np.int64))) * b.num_kv_heads * 2 * b.head_dim * elem[b.kv_dtype]
+    nblk = np.sum((b.ctx_len.astype(np.int64) + 15) // 16)
+    scales = float(nblk) * b.num_kv_heads * 2 * 4 if b.kv_dtype == "fp8" else 0.0
+    qo = float(b.total_q) * b.num_q_heads * b.head_dim * (elem[b.q_dtype] + elem[b.out_dtype])
+    return kv + scales + qo + float(nblk) * 4
+
+
+def prefill_flops(b) -> float:
+    q = b.q_len.astype(np.int64)
+    ctx = b.ctx_len.astype(np.int64)
+    pre = q > 1
+    # rows j attend pos_j + 1 keys: sum = q*(ctx-q) + q(q+1)/2
+    keys = (q * (ctx - q) + q * (q + 1) // 2)[pre]
+    return float(4 * b.head_dim * b.num_q_heads * keys.sum())
+
+
+def request_records(b, aug):
+    """Scheduler view of the batch: prefill chunks as waiting requests with
+    pending tokens, decodes as running requests."""
+    recs = np.zeros(b.num_reqs, aug.REQUEST_DTYPE)
+    for r in range(b.num_reqs):
+        q, ctx = int(b.q_len[r]), int(b.ctx_len[r])
+        rec = recs[r]
+        rec["id"] = r
+        rec["arrival"] = 0.001 * r
+        rec["last_sched"] = -1.0
+        rec["seg"] = 1
+        rec["seg_prefill"] = ctx if q == 1 else ctx
+        rec["pred_out"] = 64
+        rec["ctx_len"] = ctx - q
+        rec["pending"] = q if q > 1 else 0
+        rec["state"] = aug.AUG_WAITING if q > 1 else aug.AUG_RUNNING
+        rec["blocks_on_gpu"] = (ctx - q + 15) // 16 if q > 1 else (ctx + 15) // 16
+    return recs
+
+
+def cpu_baseline(b, budget_s: float = 15.0):
+    """Time the oracle on a prefix of the batch's requests (about budget_s of
+    CPU work), reported in query tokens per second."""
+    from oracle import attention as oa
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = len(os.sched_getaffinity(0))
+    order = list(range(b.num_reqs))
+    done_rows, t_used, n_done = 0, 0.0, 0
+    for r in order:
+        t0 = time.perf_counter()
+        oa.attention_for(b, requests=[r])
+        t_used += time.perf_counter() - t0
+        done_rows += int(b.q_len[r])
+        n_done += 1
+        if t_used >= budget_s:
+            break
+    return {"value": done_rows / t_used, "unit": "query-tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"first {n_done} of {b.num_reqs} requests ({done_rows} query rows), float64 numpy, "
+                      f"{t_used:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="decode-8b", choices=sorted(WORKLOADS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--kv-split", type=int, default=0, help="keys per decode work item (0: planner's choice)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the step needs no "
+                                   "collectives and multi-GPU runs are not part of it",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    import paper_2512_04013_amd as aug
+    from paper_2512_04013_amd import runtime as rt
+    import synth
+
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    cfg = WORKLOADS[args.workload]
+    t0 = time.time()
+    b = synth.make_config(cfg, seed=args.seed)
+    log(f"workload {b.name}: {b.num_reqs} requests, {b.total_q} query rows, "
+        f"{int(b.ctx_len.sum())} context tokens ({time.time() - t0:.1f} s to generate)")
+    shape, kv, q, bids = rt.upload_batch(b, device=dev)
+    torch.cuda.synchronize()
+
+    recs = request_records(b, aug)
+    used_blocks = int(np.sum((b.ctx_len.astype(np.int64) + 15) // 16))
+    free_blocks = b.num_pool_blocks - used_blocks
+    params = aug.former_params(t_max=2048, beta_low=0.5, beta_high=1.0, chunk_cap=512)
+    stream = torch.cuda.current_stream(dev)
+    plan_dev = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+    ws_dev = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    out = torch.empty((b.total_q, b.num_q_heads, b.head_dim),
+                      dtype=torch.float32 if b.out_dtype == "f32" else torch.bfloat16, device=dev)
+    ev = []
+
+    def step(i, timed):
+        now = 1.0 + 0.02 * i
+        formed = aug.aug_form_batch(recs, free_blocks, now, params)
+        sel = np.sort(formed["ids"]).astype(np.int64)          # slot order of the selected requests
+        q_len = np.zeros(b.num_reqs, np.int32)
+        q_len[formed["ids"]] = formed["q_len"]
+        assert np.array_equal(q_len[sel], b.q_len[sel]), "former must select the generated batch"
+        assert len(sel) == b.num_reqs, "the synthetic batch is sized to fit one budget"
+        q_start = np.zeros(len(sel) + 1, np.int32)
+        q_start[1:] = np.cumsum(q_len[sel])
+        info, plan = aug.aug_attn_plan(shape, q_start, b.ctx_len, b.bt_start, kv.num_pool_blocks,
+                                       None, kv_split_tokens=args.kv_split)
+        host = torch.from_numpy(plan).pin_memory()
+        plan_dev[:plan.size].copy_(host, non_blocking=True)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        aug.aug_attn_mixed(shape, info, plan_dev, q, kv.k_cache, kv.v_cache, kv.k_scale, kv.v_scale,
+                           bids, kv.num_pool_blocks, out, ws_dev, stream=stream.cuda_stream)
+        e1.record(stream)
+        if timed:
+            ev.append((e0, e1))
+        return info
+
+    info = None
+    for i in range(args.warmup):
+        info = step(i, False)
+    torch.cuda.synchronize()
+    log(f"plan: {info.num_items} items ({info.num_prefill_items} tiles), {info.num_merge_groups} merge "
+        f"groups, split {info.kv_split_tokens} keys")
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = 1e3 * elapsed / args.steps
+    attn_ms = float(np.mean([a.elapsed_time(c) for a, c in ev]))
+    rows = b.total_q
+    value = rows / (elapsed / args.steps)
+
+    nbytes = algorithmic_bytes(b)
+    flops = prefill_flops(b)
+    achieved_gbs = nbytes / (attn_ms * 1e-3) / 1e9
+    roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "kernel": "aug_attn_mixed launches (attention + split-K merge)",
+            "algorithmic_bytes_per_launch": int(nbytes), "launch_ms": round(attn_ms, 4)}
+    if flops > 0:
+        roof["prefill_mfma_tflops"] = round(flops / (attn_ms * 1e-3) / 1e12, 2)
+
+    result = {
+        "metric": "mixed-batch attn query-tokens/s + % peak HBM GB/s (decode) / % MFMA (prefill)",
+        "value": round(value, 1), "unit": "query-tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": b.kv_dtype, "data": "synthetic",
+        "config": {"workload": b.name, "requests": b.num_reqs, "query_rows": rows,
+                   "context_tokens": int(b.ctx_len.sum()), "q_heads": b.num_q_heads,
+                   "kv_heads": b.num_kv_heads, "head_dim": b.head_dim, "block_size": 16,
+                   "kv_split_tokens": int(info.kv_split_tokens), "seed": args.seed},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline(b, args.cpu_budget_s)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

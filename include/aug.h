@@ -1,0 +1,285 @@
+/*
+ * aug.h - C ABI of the mixed-batch serving step for augmented-LLM requests
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * The scheduler described in "AugServe: Adaptive Request Scheduling for
+ * Augmented LLM Inference Serving" (arXiv 2512.04013) forms, every engine
+ * iteration, a batch of requests that are prefilling a prompt, prefilling the
+ * tokens an external call returned, recomputing a discarded context, or
+ * decoding (request lifecycle, Eq. 1; Algorithm 1, steps (3)-(5)). Requests
+ * paused on an external call keep their KV cache on the GPU, park it in host
+ * memory, or discard it (context-handling policies, Appendix B). This library
+ * runs the data-parallel work of one such iteration:
+ *
+ *   aug_form_batch    host: token budget (Eq. token), cost and priority
+ *                     (Eqs. cost, c_fb, c_ik_new, value, theta), Waste policy
+ *                     choice (Appendix B) and greedy packing (Algorithm 1 (4))
+ *   aug_attn_plan     host: validates a formed batch and writes the work list
+ *   aug_attn_mixed    device: one launch of paged, causal, grouped-query
+ *                     attention over every chunked-prefill row and decode row
+ *                     of the batch (plus a split-K merge launch when needed)
+ *   aug_kv_park       device -> pinned host: swap-out of KV blocks
+ *   aug_kv_resume     pinned host -> device: swap-in into (new) KV blocks
+ *
+ * Conventions
+ *  - Every buffer belongs to the caller. The library allocates nothing and
+ *    keeps no state between calls.
+ *  - "device" pointers are HIP device memory of the current device; "host"
+ *    pointers are ordinary host memory unless "pinned" is stated (then it must
+ *    come from hipHostMalloc or an equivalent page-locked allocation).
+ *  - `stream` is a hipStream_t (NULL = the null stream). Device calls validate
+ *    their arguments on the host, then enqueue work and return without
+ *    waiting. A validation error enqueues nothing.
+ *  - Errors are returned as aug_status; aug_last_error() gives a message for
+ *    the most recent failing call of the calling thread.
+ *  - No C++ exception crosses this interface.
+ */
+#ifndef AUG_H
+#define AUG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AUG_OK = 0,
+  AUG_ERR_INVALID = -1,      /* an argument is out of its documented range */
+  AUG_ERR_UNSUPPORTED = -2,  /* a valid combination this build does not run */
+  AUG_ERR_NO_SPACE = -3,     /* a caller buffer is too small */
+  AUG_ERR_HIP = -4           /* the HIP runtime reported an error */
+} aug_status;
+
+typedef enum { AUG_F32 = 0, AUG_BF16 = 1, AUG_FP8_E4M3FN = 2 } aug_dtype;
+
+/* Request queues of Algorithm 1: running, swapped, waiting, paused. */
+typedef enum { AUG_WAITING = 0, AUG_RUNNING = 1, AUG_SWAPPED = 2, AUG_PAUSED = 3 } aug_state;
+
+/* Context-handling policies (set Pi), in the order the paper lists them in
+ * the Waste minimisation of Appendix B; that order breaks ties. */
+typedef enum { AUG_POL_NONE = 0, AUG_PRESERVE = 1, AUG_DISCARD = 2, AUG_SWAP = 3 } aug_policy;
+
+/* ------------------------------------------------------------------------ */
+/* Attention                                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Shape of one attention layer.
+ *   num_q_heads % num_kv_heads == 0; query head h reads KV head
+ *   h / (num_q_heads / num_kv_heads) (grouped-query attention).
+ *   head_dim: 64 or 128.  block_size: 16 (tokens per KV block).
+ *   Supported dtype sets (q, kv, out): (F32, F32, F32), (BF16, BF16, BF16),
+ *   (BF16, FP8_E4M3FN, BF16).
+ *   softmax_scale: multiplies q.k before the softmax (typically 1/sqrt(head_dim)). */
+typedef struct {
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t block_size;
+  int32_t q_dtype;
+  int32_t kv_dtype;
+  int32_t out_dtype;
+  float softmax_scale;
+} aug_attn_shape;
+
+/* A formed batch, in HOST memory.
+ *   q_start[num_reqs+1]: rows of request r are q_start[r] .. q_start[r+1]-1 of
+ *     Q and O ([rows][num_q_heads][head_dim], row-major); q_start[0] == 0 and
+ *     every request has at least one row.
+ *   ctx_len[num_reqs]: keys of request r, this step's rows included; row j of
+ *     request r sits at position ctx_len[r] - q_len + j and attends keys
+ *     0 .. that position (causal, aligned at the end of the context).
+ *     ctx_len[r] >= q_len(r).
+ *   bt_start[num_reqs+1]: request r's KV blocks are
+ *     block_ids[bt_start[r] .. bt_start[r+1]-1]; it must list at least
+ *     ceil(ctx_len[r] / block_size) of them; only that many are read.
+ *   block_ids: host copy of the block table, used only to range-check it
+ *     against num_pool_blocks; may be NULL to skip that check (the kernels
+ *     still never read outside the pool).
+ */
+typedef struct {
+  int32_t num_reqs;
+  const int32_t* q_start;
+  const int32_t* ctx_len;
+  const int32_t* bt_start;
+  const int32_t* block_ids;
+  int32_t num_pool_blocks;
+} aug_batch_desc;
+
+/* Sizes the planner derived for one batch. */
+typedef struct {
+  int64_t plan_bytes;        /* bytes of the plan image */
+  int64_t workspace_bytes;   /* device workspace aug_attn_mixed needs */
+  int32_t num_items;         /* work items of the attention launch */
+  int32_t num_prefill_items; /* of which chunked-prefill tiles */
+  int32_t num_merge_groups;  /* (request, KV head) pairs whose keys are split */
+  int32_t num_partials;      /* split-K partial results */
+  int32_t kv_split_tokens;   /* keys per decode work item (multiple of block_size) */
+  int32_t total_rows;        /* q_start[num_reqs] */
+  int32_t num_reqs;
+  int32_t reserved;
+} aug_attn_plan_info;
+
+/* Validate a formed batch and write its work list ("plan image") to
+ * plan_host, which needs info->plan_bytes bytes (call once with
+ * plan_host == NULL to obtain the sizes only). The image is position
+ * independent: copy it verbatim to device memory and pass that copy to
+ * aug_attn_mixed with the same `info`. kv_split_tokens <= 0 lets the planner
+ * choose the decode split (keys per work item); a positive value is rounded
+ * up to a multiple of block_size. Pure host code; deterministic.
+ * Errors: AUG_ERR_INVALID (shape, monotonicity, ctx_len < q_len, too few
+ * blocks, block id outside the pool), AUG_ERR_UNSUPPORTED (dtype set,
+ * head_dim, block_size), AUG_ERR_NO_SPACE (plan_cap < plan_bytes). */
+aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batch,
+                         int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
+                         aug_attn_plan_info* info);
+
+/* Mixed-batch paged attention: for every row of every request of the planned
+ * batch, O = softmax(softmax_scale * q K^T, causal) V over the request's
+ * paged keys (see aug_batch_desc). Device memory:
+ *   plan_dev   the plan image of aug_attn_plan (info->plan_bytes bytes)
+ *   q          [total_rows][num_q_heads][head_dim], q_dtype
+ *   k_cache,   [num_pool_blocks][num_kv_heads][block_size][head_dim], kv_dtype
+ *   v_cache
+ *   k_scale,   [num_pool_blocks][num_kv_heads] float32, dequantisation scale of
+ *   v_scale    each fp8 block (value = code * scale); NULL unless kv is fp8
+ *   block_ids  the block table (CSR payload of aug_batch_desc)
+ *   out        [total_rows][num_q_heads][head_dim], out_dtype
+ *   workspace  >= info->workspace_bytes bytes (split-K partials); contents on
+ *              entry do not matter
+ * Slots past a request's context and blocks it does not list never influence
+ * its output, whatever they hold. Enqueued on `stream`; one kernel launch,
+ * plus a second small launch that merges split-K partials when
+ * info->num_merge_groups > 0.
+ * Errors: AUG_ERR_INVALID (NULL pointers, info/shape mismatch),
+ * AUG_ERR_NO_SPACE (workspace_bytes too small), AUG_ERR_HIP (launch). */
+aug_status aug_attn_mixed(const aug_attn_shape* shape, const aug_attn_plan_info* info,
+                          const void* plan_dev, const void* q, const void* k_cache,
+                          const void* v_cache, const float* k_scale, const float* v_scale,
+                          const int32_t* block_ids, int32_t num_pool_blocks, void* out,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Park / resume (Swap policy: swap-out during an external call, swap-in     */
+/* when it returns; Appendix B, Algorithm 1 step (2))                         */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of one parked block record: K[block] then V[block]
+ * (num_kv_heads * block_size * head_dim elements each, the pool's own bit
+ * patterns), then, for fp8 caches, k_scale[block] and v_scale[block]
+ * (num_kv_heads float32 each). Returns 0 for an invalid shape. */
+size_t aug_kv_record_bytes(const aug_attn_shape* shape);
+
+/* Park n_blocks blocks: host_dst (pinned, >= n_blocks * record bytes) receives
+ * the records of block_ids_dev[0..n_blocks-1] in that order. Data moves
+ * through `staging` (device, >= one record; larger staging means fewer,
+ * larger copies): a gather kernel fills it, then an asynchronous copy drains
+ * it to host_dst, chunk after chunk, all on `stream`. host_dst is complete
+ * once the stream reaches the end of this call's work.
+ * block_ids_dev: device int32[n_blocks]. block_ids_host: optional host copy,
+ * range-checked against num_pool_blocks when given; the kernel itself skips
+ * (and leaves undefined) any record whose id is outside the pool.
+ * Errors: AUG_ERR_INVALID, AUG_ERR_NO_SPACE (host_bytes, staging_bytes),
+ * AUG_ERR_HIP. */
+aug_status aug_kv_park(const aug_attn_shape* shape, const void* k_cache, const void* v_cache,
+                       const float* k_scale, const float* v_scale,
+                       const int32_t* block_ids_dev, const int32_t* block_ids_host,
+                       int32_t n_blocks, int32_t num_pool_blocks, void* host_dst,
+                       size_t host_bytes, void* staging, size_t staging_bytes, void* stream);
+
+/* Resume n_blocks records from host_src (pinned, as written by aug_kv_park)
+ * into the pool blocks block_ids_dev[0..n_blocks-1] (any blocks: a resumed
+ * request usually lands elsewhere than it was). Same staging scheme in the
+ * other direction. Ids outside the pool are skipped by the kernel.
+ * Errors as aug_kv_park. */
+aug_status aug_kv_resume(const aug_attn_shape* shape, void* k_cache, void* v_cache,
+                         float* k_scale, float* v_scale, const int32_t* block_ids_dev,
+                         const int32_t* block_ids_host, int32_t n_blocks,
+                         int32_t num_pool_blocks, const void* host_src, size_t host_bytes,
+                         void* staging, size_t staging_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Batch former (host)                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* One request R_i as the scheduler sees it (symbols of the paper's notation
+ * table). Times are seconds on the caller's clock. */
+typedef struct {
+  int64_t id;             /* unique */
+  double arrival;
+  double last_sched;      /* last time it was scheduled; < 0 if never */
+  double pred_call;       /* tau_hat^call of the call ending this segment (s) */
+  double pause_start;     /* PAUSED: when the current wait began */
+  int32_t state;          /* aug_state */
+  int32_t seg;            /* k, 1 for the first segment */
+  int32_t prev_policy;    /* p_{i,k-1}: policy realised during the last wait (k >= 2) */
+  int32_t cur_policy;     /* PAUSED: policy chosen for the current wait */
+  int32_t seg_ctx;        /* L: context tokens at the segment start (before returned tokens) */
+  int32_t seg_prefill;    /* tokens prefilled in this segment: prompt (k = 1) or returned (k >= 2) */
+  int32_t pred_out;       /* l_hat^out: tokens predicted for this segment, >= 1 */
+  int32_t has_next_call;  /* 1 if the segment ends in an external call */
+  int32_t ctx_len;        /* tokens whose KV the request holds now */
+  int32_t pending;        /* tokens to prefill before its next decode (prompt, returned, recompute) */
+  int32_t blocks_on_gpu;  /* pool blocks it holds now */
+  int32_t reserved;
+} aug_request;
+
+typedef struct {
+  double beta;            /* aging factor of Eq. value; w is in milliseconds */
+  double beta_low;        /* budget clip: [floor(beta_low*t_max), floor(beta_high*t_max)] */
+  double beta_high;
+  double t_iter;          /* seconds per engine iteration in the space-time cost */
+  double fwd_a;           /* tau_fwd(L) = fwd_a + fwd_b * L  (Waste of Discard) */
+  double fwd_b;
+  double swap_s_per_tok;  /* tau_swap(L) = swap_s_per_tok * L */
+  int64_t n_fwd_max;      /* N_max^fwd of the Swap Waste */
+  int32_t t_max;          /* T_max, reference token budget */
+  int32_t chunk_cap;      /* most prefill tokens one request takes per iteration */
+  int32_t block_size;     /* tokens per pool block */
+  int32_t skip_instead_of_break; /* 0: stop at the first request that does not fit */
+} aug_former_params;
+
+/* Output of aug_form_batch. The caller sets `cap` and the array pointers; each
+ * id/q_len/theta array must hold `cap` entries, policy_out and cost_out one
+ * entry per input request (either may be NULL). */
+typedef struct {
+  int32_t cap;
+  int32_t budget;         /* B_token after clipping */
+  int32_t n_sched;        /* scheduled requests, in rank order */
+  int32_t n_resume;       /* scheduled requests that were swapped out */
+  int32_t n_park;         /* paused Swap requests evicted to host memory */
+  int32_t n_free;         /* paused Discard requests whose blocks are freed */
+  int64_t* ids;           /* [cap] scheduled ids */
+  int32_t* q_len;         /* [cap] tokens each scheduled request runs */
+  double* theta;          /* [cap] priority at formation */
+  int64_t* resume_ids;    /* [cap] */
+  int64_t* park_ids;      /* [cap] */
+  int64_t* free_ids;      /* [cap] */
+  int32_t* policy_out;    /* [n] predicted policy per input (AUG_POL_NONE if not a candidate) */
+  double* cost_out;       /* [n] C_{i,k} per input (0 if not a candidate) */
+} aug_batch_plan;
+
+/* Form one iteration's batch (Algorithm 1, steps (3)-(4)) from n requests and
+ * free_blocks free pool blocks at time `now`. Deterministic, pure host code in
+ * IEEE double precision with a fixed operation order.
+ * Errors: AUG_ERR_INVALID (NULL pointers, pred_out < 1 for a candidate,
+ * negative sizes, t_iter <= 0, chunk_cap < 1, block_size < 1, unknown state),
+ * AUG_ERR_NO_SPACE (more than `cap` entries in any output list). */
+aug_status aug_form_batch(const aug_request* reqs, int32_t n, int64_t free_blocks, double now,
+                          const aug_former_params* params, aug_batch_plan* out);
+
+/* ------------------------------------------------------------------------ */
+
+/* Static name of a status code. */
+const char* aug_status_string(aug_status s);
+/* Message of the calling thread's most recent failing call ("" if none). */
+const char* aug_last_error(void);
+/* Version of this ABI: (major << 16) | minor. */
+int32_t aug_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AUG_H */

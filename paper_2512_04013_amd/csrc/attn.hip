@@ -1,0 +1,673 @@
+// Mixed-batch paged attention for gfx950 (MI355X).
+//
+// One launch runs every work item of a plan (plan_format.h):
+//
+//  * Row items (decodes; prefill rows of dtype sets without a tile path): one
+//    query row and the G query heads that share one KV head, against a span of
+//    that request's keys. A 256-thread workgroup streams the span's 16-token
+//    blocks, each wave its own blocks (wave w takes blocks w, w+4, ...). A
+//    block of one KV head is 16 contiguous rows of head_dim elements, so a
+//    wave reads it with fully coalesced 16-byte (8-byte for fp8) lane loads:
+//    LPT lanes cover one token row, 64/LPT tokens per load instruction. Scores
+//    are reduced across the LPT lanes of a token with DPP row operations, the
+//    softmax is online in the log2 domain, and every lane group keeps its own
+//    running (max, sum, output) state; the states are merged across lane
+//    groups with cross-lane shuffles and across waves through LDS. Each KV byte
+//    is read once for all G heads (grouped-query sharing). Arithmetic runs on
+//    the vector ALUs in fp32.
+//  * Tile items (bf16 chunked prefill): 128 query rows (positions x group
+//    heads) of one chunk, causal against keys 0 .. last row's position. K and V
+//    are staged through LDS 64 keys at a time (V transposed on the way in), and
+//    both products run on bf16 MFMA 32x32x16 with fp32 accumulation:
+//    S^T = K Q^T puts one query row per lane column, so the row max/sum are
+//    lane-local plus one exchange between the two lane halves, and
+//    O^T = V^T P^T takes P straight from the S^T accumulators.
+//
+// Keys past a request's context (tail of its last block) and blocks it does
+// not list never reach the arithmetic: their loads are skipped (zero-filled)
+// and their scores masked, so NaN or garbage in unused slots cannot leak.
+// Block ids outside the pool are treated the same way (never dereferenced).
+//
+// Split-K: a row item whose request was split writes an unnormalised partial
+// (o, m, l) to the workspace; a second, small launch merges the partials of
+// each (row, KV head) by log-sum-exp.
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "aug.h"
+#include "plan_format.h"
+#include "status.h"
+
+namespace aug {
+aug_status check_shape(const aug_attn_shape* s, const char* who);
+}
+
+namespace {
+
+using aug::kBlock;
+using aug::MergeGroup;
+using aug::WorkItem;
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
+constexpr int kThreads = 256;
+
+enum : int { KV_F32 = 0, KV_BF16 = 1, KV_FP8 = 2 };
+
+struct AttnArgs {
+  const WorkItem* items;
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  const float* k_scale;
+  const float* v_scale;
+  const int32_t* block_ids;
+  void* out;
+  float* partials;
+  int32_t num_pool_blocks;
+  int32_t hq;
+  int32_t hkv;
+  float scale_log2;    // softmax_scale * log2(e)
+};
+
+// ---------------------------------------------------------------------------
+// small helpers
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);   // round to nearest even (inputs are finite)
+  return u >> 16;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over aligned groups of LANES lanes (4, 8, 16 or 32); every lane of a
+// group receives the group's sum.
+template <int LANES>
+__device__ __forceinline__ float group_sum(float v) {
+  v += dpp<0xB1>(v);                  // quad_perm [1,0,3,2]: lane ^ 1
+  v += dpp<0x4E>(v);                  // quad_perm [2,3,0,1]: lane ^ 2
+  if constexpr (LANES >= 8) v += dpp<0x141>(v);   // row_half_mirror: pairs quads of 8
+  if constexpr (LANES >= 16) v += dpp<0x140>(v);  // row_mirror: pairs halves of 16
+  if constexpr (LANES >= 32) v += __shfl_xor(v, 16);
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// KV element formats for the row path
+// ---------------------------------------------------------------------------
+
+template <int KVT> struct KvFmt;
+template <> struct KvFmt<KV_F32> {
+  static constexpr int VEC = 4;       // elements per lane load (16 bytes)
+  using raw_t = uint4;
+  __device__ static void to_f32(const raw_t& r, float* f) {
+    f[0] = __uint_as_float(r.x); f[1] = __uint_as_float(r.y);
+    f[2] = __uint_as_float(r.z); f[3] = __uint_as_float(r.w);
+  }
+};
+template <> struct KvFmt<KV_BF16> {
+  static constexpr int VEC = 8;       // 16 bytes
+  using raw_t = uint4;
+  __device__ static void to_f32(const raw_t& r, float* f) {
+    f[0] = bf16_lo(r.x); f[1] = bf16_hi(r.x); f[2] = bf16_lo(r.y); f[3] = bf16_hi(r.y);
+    f[4] = bf16_lo(r.z); f[5] = bf16_hi(r.z); f[6] = bf16_lo(r.w); f[7] = bf16_hi(r.w);
+  }
+};
+template <> struct KvFmt<KV_FP8> {
+  static constexpr int VEC = 8;       // 8 bytes
+  using raw_t = uint2;
+  __device__ static void to_f32(const raw_t& r, float* f) {
+    // gfx950 converts OCP E4M3FN codes exactly to fp32, two at a time
+    auto a = __builtin_amdgcn_cvt_pk_f32_fp8(r.x, false);
+    auto b = __builtin_amdgcn_cvt_pk_f32_fp8(r.x, true);
+    auto c = __builtin_amdgcn_cvt_pk_f32_fp8(r.y, false);
+    auto d = __builtin_amdgcn_cvt_pk_f32_fp8(r.y, true);
+    f[0] = a[0]; f[1] = a[1]; f[2] = b[0]; f[3] = b[1];
+    f[4] = c[0]; f[5] = c[1]; f[6] = d[0]; f[7] = d[1];
+  }
+};
+
+template <int QT>
+__device__ __forceinline__ void load_q(const void* q, int64_t off, float* f) {
+  if constexpr (QT == AUG_F32) {
+    const float4 v = *reinterpret_cast<const float4*>(static_cast<const float*>(q) + off);
+    f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w;
+  } else {
+    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(q) + off);
+    f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
+    f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z); f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
+  }
+}
+
+template <int OT>
+__device__ __forceinline__ void store_out(void* out, int64_t off, float v) {
+  if constexpr (OT == AUG_F32) {
+    static_cast<float*>(out)[off] = v;
+  } else {
+    static_cast<uint16_t*>(out)[off] = static_cast<uint16_t>(f32_to_bf16_bits(v));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// row items (VALU)
+// ---------------------------------------------------------------------------
+
+template <int KVT, int D, int G, int QT, int OT>
+__device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
+  using F = KvFmt<KVT>;
+  constexpr int VEC = F::VEC;
+  constexpr int LPT = D / VEC;        // lanes per token row
+  constexpr int TPI = 64 / LPT;       // tokens per load instruction
+  constexpr int NLD = kBlock / TPI;   // load instructions per 16-token block
+  static_assert(LPT >= 4 && LPT <= 32 && NLD >= 1, "row-path lane mapping");
+  static_assert(QT == AUG_BF16 ? VEC == 8 : VEC == 4, "Q vector width follows KV width");
+  using elem_t = typename F::raw_t;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int dl = lane % LPT;
+  const int tsub = lane / LPT;
+  const int d0 = dl * VEC;
+  const int kvh = it.kind_kvh & 0xFFFF;
+
+  float q[G][VEC];
+  {
+    const int64_t qoff = (static_cast<int64_t>(it.q_row0) * a.hq + static_cast<int64_t>(kvh) * G) * D + d0;
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      load_q<QT>(a.q, qoff + static_cast<int64_t>(h) * D, q[h]);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) q[h][e] *= a.scale_log2;
+    }
+  }
+
+  float m[G], l[G], o[G][VEC];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    m[h] = kNegBig;
+    l[h] = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[h][e] = 0.f;
+  }
+
+  const int blk0 = it.key_begin / kBlock;
+  const int nblk = (it.key_end - it.key_begin + kBlock - 1) / kBlock;
+  const int64_t head_stride = static_cast<int64_t>(kBlock) * D;   // elements of one (block, head)
+
+  for (int bi = wave; bi < nblk; bi += kThreads / 64) {
+    const int blk = blk0 + bi;
+    const int bid = __builtin_amdgcn_readfirstlane(a.block_ids[it.bt_off + blk]);
+    const bool bid_ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
+    const int tok0 = blk * kBlock;
+    const int64_t base = (static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride + d0;
+
+    elem_t kraw[NLD], vraw[NLD];
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int t = i * TPI + tsub;
+      if (bid_ok) {
+        kraw[i] = *reinterpret_cast<const elem_t*>(
+            static_cast<const char*>(a.k_cache) + (base + static_cast<int64_t>(t) * D) * (KVT == KV_F32 ? 4 : KVT == KV_BF16 ? 2 : 1));
+        vraw[i] = *reinterpret_cast<const elem_t*>(
+            static_cast<const char*>(a.v_cache) + (base + static_cast<int64_t>(t) * D) * (KVT == KV_F32 ? 4 : KVT == KV_BF16 ? 2 : 1));
+      } else {
+        kraw[i] = elem_t{};
+        vraw[i] = elem_t{};
+      }
+    }
+    float ksc = 1.f, vsc = 1.f;
+    if constexpr (KVT == KV_FP8) {
+      if (bid_ok) {
+        ksc = a.k_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
+        vsc = a.v_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
+      }
+    }
+
+    float s[NLD][G];
+    bool valid[NLD];
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      valid[i] = bid_ok && (tok0 + i * TPI + tsub) < it.key_end;
+      float kf[VEC];
+      F::to_f32(kraw[i], kf);
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        float acc = 0.f;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc += q[h][e] * kf[e];
+        acc = group_sum<LPT>(acc) * ksc;
+        s[i][h] = valid[i] ? acc : -INFINITY;
+      }
+    }
+
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float mb = s[0][h];
+#pragma unroll
+      for (int i = 1; i < NLD; ++i) mb = fmaxf(mb, s[i][h]);
+      const float mn = fmaxf(m[h], mb);
+      const float alpha = __builtin_amdgcn_exp2f(m[h] - mn);
+      m[h] = mn;
+      float psum = 0.f;
+      float p[NLD];
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        p[i] = __builtin_amdgcn_exp2f(s[i][h] - mn);
+        psum += p[i];
+      }
+      l[h] = l[h] * alpha + psum;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[h][e] *= alpha;
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) p[i] *= vsc;
+      // accumulate p_i * v_i (values of masked tokens are never touched)
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        float vf[VEC];
+        F::to_f32(vraw[i], vf);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[h][e] += valid[i] ? p[i] * vf[e] : 0.f;
+      }
+    }
+  }
+
+  // merge the TPI lane groups of this wave (lanes with equal dl)
+#pragma unroll
+  for (int mask = LPT; mask < 64; mask <<= 1) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float mo = __shfl_xor(m[h], mask);
+      const float lo = __shfl_xor(l[h], mask);
+      const float mn = fmaxf(m[h], mo);
+      const float a1 = __builtin_amdgcn_exp2f(m[h] - mn);
+      const float a2 = __builtin_amdgcn_exp2f(mo - mn);
+      l[h] = l[h] * a1 + lo * a2;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[h][e] = o[h][e] * a1 + __shfl_xor(o[h][e], mask) * a2;
+      m[h] = mn;
+    }
+  }
+
+  // merge the four waves through LDS: [wave][head][D + 2]
+  constexpr int ROW = D + 2;
+  if (tsub == 0) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float* dst = lds + (wave * G + h) * ROW;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) dst[d0 + e] = o[h][e];
+      if (dl == 0) {
+        dst[D] = m[h];
+        dst[D + 1] = l[h];
+      }
+    }
+  }
+  __syncthreads();
+  constexpr int NW = kThreads / 64;
+  for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
+    const int h = idx / D;
+    const int d = idx % D;
+    float mw[NW];
+    float mx = kNegBig;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      mw[w] = lds[(w * G + h) * ROW + D];
+      mx = fmaxf(mx, mw[w]);
+    }
+    float ls = 0.f, os = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float f = __builtin_amdgcn_exp2f(mw[w] - mx);
+      ls += lds[(w * G + h) * ROW + D + 1] * f;
+      os += lds[(w * G + h) * ROW + d] * f;
+    }
+    if (it.part < 0) {
+      const int64_t off = (static_cast<int64_t>(it.q_row0) * a.hq + static_cast<int64_t>(kvh) * G + h) * D + d;
+      store_out<OT>(a.out, off, os / ls);
+    } else {
+      float* pp = a.partials + static_cast<int64_t>(it.part) * aug::partial_floats(G, D);
+      pp[h * D + d] = os;
+      if (d == 0) {
+        pp[G * D + h] = mx;
+        pp[G * D + G + h] = ls;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// tile items (bf16 MFMA)
+// ---------------------------------------------------------------------------
+
+template <int D>
+struct TileLds {
+  static constexpr int KS = D + 8;    // K row stride (elements): 16-byte aligned, conflict-free reads
+  static constexpr int VS = 64 + 4;   // V^T row stride (elements)
+  static constexpr int BYTES = (64 * KS + D * VS) * 2;
+};
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+template <int D, int G, int OT>
+__device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* smem) {
+  using L = TileLds<D>;
+  constexpr int KSTEPS = D / 16;      // k-steps of S^T over head_dim
+  constexpr int DB = D / 32;          // 32-dim blocks of O^T
+  constexpr int CPR = D / 8;          // 16-byte chunks per key row
+  constexpr int KPT = 64 * CPR / kThreads;   // keys staged per thread (4 or 2)
+  static_assert(KPT == 2 || KPT == 4, "tile staging map");
+  uint16_t* ks = reinterpret_cast<uint16_t*>(smem);
+  uint16_t* vt = ks + 64 * L::KS;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int n = lane & 31;            // MFMA column: query row within the wave
+  const int hh = lane >> 5;           // lane half: which 8 of the 16 k-slots
+  const int kvh = it.kind_kvh & 0xFFFF;
+  const int row = wave * 32 + n;
+  const int p = row / G;
+  const int gh = row % G;
+  const bool row_ok = p < it.n_rows;
+  const int pos = it.pos0 + p;
+  const uint16_t* qb = static_cast<const uint16_t*>(a.q);
+
+  uint4 qreg[KSTEPS];
+  {
+    const int64_t qoff = (static_cast<int64_t>(it.q_row0 + p) * a.hq + static_cast<int64_t>(kvh) * G + gh) * D;
+#pragma unroll
+    for (int s = 0; s < KSTEPS; ++s)
+      qreg[s] = row_ok ? *reinterpret_cast<const uint4*>(qb + qoff + 16 * s + 8 * hh) : uint4{0, 0, 0, 0};
+  }
+
+  f32x16_t acc_o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc_o[db][e] = 0.f;
+  float m_run = kNegBig, l_run = 0.f;
+  const float c = a.scale_log2;
+
+  const int tc = threadIdx.x % CPR;
+  const int tk = threadIdx.x / CPR;
+  const int key_end = it.key_end;
+  const int ntiles = (key_end + 63) / 64;
+  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
+  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
+  const int64_t head_stride = static_cast<int64_t>(kBlock) * D;
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = t * 64;
+    uint4 kr[KPT], vr[KPT];
+#pragma unroll
+    for (int u = 0; u < KPT; ++u) {
+      const int tok = k0 + tk * KPT + u;
+      kr[u] = uint4{0, 0, 0, 0};
+      vr[u] = uint4{0, 0, 0, 0};
+      if (tok < key_end) {
+        const int bid = a.block_ids[it.bt_off + (tok >> 4)];
+        if (static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks)) {
+          const int64_t off = (static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride +
+                              static_cast<int64_t>(tok & 15) * D + 8 * tc;
+          kr[u] = *reinterpret_cast<const uint4*>(kc + off);
+          vr[u] = *reinterpret_cast<const uint4*>(vc + off);
+        }
+      }
+    }
+    __syncthreads();   // the previous tile's LDS reads are done
+#pragma unroll
+    for (int u = 0; u < KPT; ++u)
+      *reinterpret_cast<uint4*>(ks + (tk * KPT + u) * L::KS + 8 * tc) = kr[u];
+    // V^T: element e of each of this thread's KPT keys goes to row 8*tc+e
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint32_t w[KPT];
+#pragma unroll
+      for (int u = 0; u < KPT; ++u) {
+        const uint32_t word = (&vr[u].x)[e >> 1];
+        w[u] = (e & 1) ? (word >> 16) : (word & 0xFFFFu);
+      }
+      uint16_t* dst = vt + (8 * tc + e) * L::VS + tk * KPT;
+      if constexpr (KPT == 4) {
+        *reinterpret_cast<uint2*>(dst) = uint2{w[0] | (w[1] << 16), w[2] | (w[3] << 16)};
+      } else {
+        *reinterpret_cast<uint32_t*>(dst) = w[0] | (w[1] << 16);
+      }
+    }
+    __syncthreads();
+
+    // S^T = K Q^T for keys k0..k0+63
+    f32x16_t sacc[2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sacc[mb][e] = 0.f;
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s) {
+        const uint4 kop = *reinterpret_cast<const uint4*>(ks + (32 * mb + n) * L::KS + 16 * s + 8 * hh);
+        sacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), as_bf16x8(qreg[s]), sacc[mb], 0, 0, 0);
+      }
+    }
+
+    // online softmax over this row's 64 keys (32 in each lane half)
+    const bool need_mask = k0 + 63 > it.pos0;
+    float smax = kNegBig;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int key = k0 + 32 * mb + 8 * i + 4 * hh + j;
+          float v = sacc[mb][4 * i + j] * c;
+          if (need_mask && key > pos) v = -INFINITY;
+          sacc[mb][4 * i + j] = v;
+          smax = fmaxf(smax, v);
+        }
+    smax = fmaxf(smax, __shfl_xor(smax, 32));
+    const float mn = fmaxf(m_run, smax);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
+    m_run = mn;
+    float psum = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float pv = __builtin_amdgcn_exp2f(sacc[mb][e] - mn);
+        sacc[mb][e] = pv;
+        psum += pv;
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc_o[db][e] *= alpha;
+
+    // O^T += V^T P^T, 16 keys per step; k-slots of lane half hh are keys
+    // {16s+4hh+j, 16s+8+4hh+j}, exactly the S^T entries this lane holds
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int mb = s >> 1;
+      const int i0 = 2 * (s & 1);
+      uint4 pw;
+      pw.x = f32_to_bf16_bits(sacc[mb][4 * i0 + 0]) | (f32_to_bf16_bits(sacc[mb][4 * i0 + 1]) << 16);
+      pw.y = f32_to_bf16_bits(sacc[mb][4 * i0 + 2]) | (f32_to_bf16_bits(sacc[mb][4 * i0 + 3]) << 16);
+      pw.z = f32_to_bf16_bits(sacc[mb][4 * i0 + 4]) | (f32_to_bf16_bits(sacc[mb][4 * i0 + 5]) << 16);
+      pw.w = f32_to_bf16_bits(sacc[mb][4 * i0 + 6]) | (f32_to_bf16_bits(sacc[mb][4 * i0 + 7]) << 16);
+      const bf16x8_t pop = as_bf16x8(pw);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const uint16_t* vrow = vt + (32 * db + n) * L::VS + 16 * s + 4 * hh;
+        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
+        const uint4 vop{lo.x, lo.y, hi.x, hi.y};
+        acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vop), pop, acc_o[db], 0, 0, 0);
+      }
+    }
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (row_ok) {
+    const float inv = 1.f / l_tot;
+    const int64_t ooff = (static_cast<int64_t>(it.q_row0 + p) * a.hq + static_cast<int64_t>(kvh) * G + gh) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int dim = 32 * db + 8 * i + 4 * hh;
+        if constexpr (OT == AUG_BF16) {
+          uint2 w;
+          w.x = f32_to_bf16_bits(acc_o[db][4 * i + 0] * inv) | (f32_to_bf16_bits(acc_o[db][4 * i + 1] * inv) << 16);
+          w.y = f32_to_bf16_bits(acc_o[db][4 * i + 2] * inv) | (f32_to_bf16_bits(acc_o[db][4 * i + 3] * inv) << 16);
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + ooff + dim) = w;
+        } else {
+          float4 w{acc_o[db][4 * i] * inv, acc_o[db][4 * i + 1] * inv, acc_o[db][4 * i + 2] * inv,
+                   acc_o[db][4 * i + 3] * inv};
+          *reinterpret_cast<float4*>(static_cast<float*>(a.out) + ooff + dim) = w;
+        }
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// kernels
+// ---------------------------------------------------------------------------
+
+template <int D, int G>
+constexpr int row_lds_bytes() { return (kThreads / 64) * G * (D + 2) * 4; }
+
+template <int KVT, int D, int G, int QT, int OT, bool TILES>
+__global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
+  constexpr int RB = row_lds_bytes<D, G>();
+  constexpr int TB = TILES ? TileLds<D>::BYTES : 0;
+  __shared__ __align__(16) unsigned char smem[RB > TB ? RB : TB];
+  const WorkItem it = a.items[blockIdx.x];
+  if constexpr (TILES) {
+    if ((it.kind_kvh >> 16) == aug::kTileItem) {
+      tile_item<D, G, OT>(it, a, smem);
+      return;
+    }
+  }
+  row_item<KVT, D, G, QT, OT>(it, a, reinterpret_cast<float*>(smem));
+}
+
+template <int D, int G, int OT>
+__global__ __launch_bounds__(kThreads) void merge_kernel(const MergeGroup* groups, const float* partials,
+                                                         void* out, int32_t hq) {
+  const MergeGroup g = groups[blockIdx.x];
+  const int64_t pf = aug::partial_floats(G, D);
+  for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
+    const int h = idx / D;
+    const int d = idx % D;
+    float mx = kNegBig;
+    for (int s = 0; s < g.n_parts; ++s) mx = fmaxf(mx, partials[(g.part0 + s) * pf + G * D + h]);
+    float ls = 0.f, os = 0.f;
+    for (int s = 0; s < g.n_parts; ++s) {
+      const float* pp = partials + (g.part0 + s) * pf;
+      const float f = __builtin_amdgcn_exp2f(pp[G * D + h] - mx);
+      ls += pp[G * D + G + h] * f;
+      os += pp[h * D + d] * f;
+    }
+    const int64_t off = (static_cast<int64_t>(g.q_row) * hq + static_cast<int64_t>(g.kvh) * G + h) * D + d;
+    store_out<OT>(out, off, os / ls);
+  }
+}
+
+template <int KVT, int D, int G, int QT, int OT>
+aug_status launch(const AttnArgs& a, const aug_attn_plan_info& info, const MergeGroup* groups,
+                  hipStream_t st) {
+  if (info.num_items > 0) {
+    if (info.num_prefill_items > 0) {
+      if constexpr (KVT == KV_BF16 && QT == AUG_BF16) {
+        hipLaunchKernelGGL((attn_kernel<KVT, D, G, QT, OT, true>), dim3(info.num_items), dim3(kThreads), 0, st, a);
+      } else {
+        return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: plan has tiles for a dtype set without them");
+      }
+    } else {
+      hipLaunchKernelGGL((attn_kernel<KVT, D, G, QT, OT, false>), dim3(info.num_items), dim3(kThreads), 0, st, a);
+    }
+    if (hipError_t e = hipGetLastError(); e != hipSuccess)
+      return aug::fail(AUG_ERR_HIP, "aug_attn_mixed: launch failed: %s", hipGetErrorString(e));
+  }
+  if (info.num_merge_groups > 0) {
+    hipLaunchKernelGGL((merge_kernel<D, G, OT>), dim3(info.num_merge_groups), dim3(kThreads), 0, st,
+                       groups, a.partials, a.out, a.hq);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess)
+      return aug::fail(AUG_ERR_HIP, "aug_attn_mixed: merge launch failed: %s", hipGetErrorString(e));
+  }
+  return AUG_OK;
+}
+
+template <int KVT, int QT, int OT>
+aug_status dispatch_dg(int d, int g, const AttnArgs& a, const aug_attn_plan_info& info,
+                       const MergeGroup* groups, hipStream_t st) {
+#define AUG_CASE(DD, GG) \
+  if (d == DD && g == GG) return launch<KVT, DD, GG, QT, OT>(a, info, groups, st);
+  if constexpr (KVT != KV_FP8) {
+    AUG_CASE(64, 1) AUG_CASE(64, 2) AUG_CASE(64, 4) AUG_CASE(64, 8)
+  }
+  AUG_CASE(128, 1) AUG_CASE(128, 2) AUG_CASE(128, 4) AUG_CASE(128, 8)
+#undef AUG_CASE
+  return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: head_dim %d with group %d", d, g);
+}
+
+}  // namespace
+
+extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_plan_info* info,
+                                     const void* plan_dev, const void* q, const void* k_cache,
+                                     const void* v_cache, const float* k_scale, const float* v_scale,
+                                     const int32_t* block_ids, int32_t num_pool_blocks, void* out,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  const char* who = "aug_attn_mixed";
+  if (aug_status st = aug::check_shape(s, who); st != AUG_OK) return st;
+  if (!info) return aug::fail(AUG_ERR_INVALID, "%s: info is NULL", who);
+  if (info->num_items < 0 || info->num_merge_groups < 0 || info->num_partials < 0 ||
+      info->plan_bytes != static_cast<int64_t>(sizeof(aug::PlanHeader)) +
+                              static_cast<int64_t>(info->num_items) * sizeof(WorkItem) +
+                              static_cast<int64_t>(info->num_merge_groups) * sizeof(MergeGroup))
+    return aug::fail(AUG_ERR_INVALID, "%s: info is inconsistent", who);
+  if (info->num_items == 0) return AUG_OK;
+  if (!plan_dev || !q || !k_cache || !v_cache || !block_ids || !out)
+    return aug::fail(AUG_ERR_INVALID, "%s: NULL device pointer", who);
+  if (s->kv_dtype == AUG_FP8_E4M3FN && (!k_scale || !v_scale))
+    return aug::fail(AUG_ERR_INVALID, "%s: fp8 KV needs k_scale and v_scale", who);
+  if (num_pool_blocks < 1) return aug::fail(AUG_ERR_INVALID, "%s: empty pool", who);
+  if (info->num_partials > 0 && (!workspace || workspace_bytes < static_cast<size_t>(info->workspace_bytes)))
+    return aug::fail(AUG_ERR_NO_SPACE, "%s: workspace %zu < %lld bytes", who, workspace_bytes,
+                     (long long)info->workspace_bytes);
+
+  AttnArgs a{};
+  const auto* base = static_cast<const unsigned char*>(plan_dev);
+  a.items = reinterpret_cast<const WorkItem*>(base + sizeof(aug::PlanHeader));
+  const auto* groups = reinterpret_cast<const MergeGroup*>(
+      base + sizeof(aug::PlanHeader) + static_cast<size_t>(info->num_items) * sizeof(WorkItem));
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.k_scale = k_scale;
+  a.v_scale = v_scale;
+  a.block_ids = block_ids;
+  a.out = out;
+  a.partials = static_cast<float*>(workspace);
+  a.num_pool_blocks = num_pool_blocks;
+  a.hq = s->num_q_heads;
+  a.hkv = s->num_kv_heads;
+  a.scale_log2 = s->softmax_scale * kLog2e;
+  const int g = s->num_q_heads / s->num_kv_heads;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (s->kv_dtype == AUG_F32) return dispatch_dg<KV_F32, AUG_F32, AUG_F32>(s->head_dim, g, a, *info, groups, st);
+  if (s->kv_dtype == AUG_BF16) return dispatch_dg<KV_BF16, AUG_BF16, AUG_BF16>(s->head_dim, g, a, *info, groups, st);
+  return dispatch_dg<KV_FP8, AUG_BF16, AUG_BF16>(s->head_dim, g, a, *info, groups, st);
+}

@@ -1,0 +1,259 @@
+// Host planner of the mixed-batch attention launch.
+//
+// It turns a formed batch (per request: query rows, context length, block
+// table) into a work list for one kernel launch:
+//  * chunked-prefill requests with bf16 Q/K/V become MFMA tiles of
+//    kTileRows query rows (positions x the G query heads of one KV head),
+//    each reading keys 0 .. its last row's position;
+//  * every other row (decodes, and prefill rows of dtype sets without an MFMA
+//    path) becomes row items: one row, the G heads of one KV head, and a span
+//    of keys; long contexts are split into spans of nearly equal length whose
+//    partial softmax states a second launch merges (split-K).
+// Items are ordered longest first so the long ones start early. The planner
+// is deterministic and validates the batch completely before any launch.
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "aug.h"
+#include "plan_format.h"
+#include "status.h"
+
+namespace aug {
+
+bool dtype_set_supported(const aug_attn_shape& s) {
+  if (s.q_dtype == AUG_F32 && s.kv_dtype == AUG_F32 && s.out_dtype == AUG_F32) return true;
+  if (s.q_dtype == AUG_BF16 && s.kv_dtype == AUG_BF16 && s.out_dtype == AUG_BF16) return true;
+  if (s.q_dtype == AUG_BF16 && s.kv_dtype == AUG_FP8_E4M3FN && s.out_dtype == AUG_BF16) return true;
+  return false;
+}
+
+bool tiles_supported(const aug_attn_shape& s) {
+  return s.q_dtype == AUG_BF16 && s.kv_dtype == AUG_BF16;
+}
+
+aug_status check_shape(const aug_attn_shape* s, const char* who) {
+  if (!s) return fail(AUG_ERR_INVALID, "%s: shape is NULL", who);
+  if (s->num_q_heads < 1 || s->num_kv_heads < 1 || s->num_q_heads % s->num_kv_heads != 0)
+    return fail(AUG_ERR_INVALID, "%s: heads %d/%d are not a positive multiple", who,
+                s->num_q_heads, s->num_kv_heads);
+  const int g = s->num_q_heads / s->num_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8)
+    return fail(AUG_ERR_UNSUPPORTED, "%s: group size %d (supported: 1, 2, 4, 8)", who, g);
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(AUG_ERR_UNSUPPORTED, "%s: head_dim %d (supported: 64, 128)", who, s->head_dim);
+  if (s->block_size != kBlock)
+    return fail(AUG_ERR_UNSUPPORTED, "%s: block_size %d (supported: 16)", who, s->block_size);
+  if (!dtype_set_supported(*s))
+    return fail(AUG_ERR_UNSUPPORTED, "%s: dtype set q=%d kv=%d out=%d", who, s->q_dtype,
+                s->kv_dtype, s->out_dtype);
+  if (s->kv_dtype == AUG_FP8_E4M3FN && s->head_dim != 128)
+    return fail(AUG_ERR_UNSUPPORTED, "%s: fp8 KV needs head_dim 128", who);
+  if (!std::isfinite(s->softmax_scale))
+    return fail(AUG_ERR_INVALID, "%s: softmax_scale is not finite", who);
+  return AUG_OK;
+}
+
+namespace {
+
+struct Sized {
+  WorkItem item;
+  int64_t weight;   // sort key: longest first
+  int64_t order;    // creation order, to keep the sort deterministic
+};
+
+int32_t choose_split(int64_t total_row_keys, int32_t requested) {
+  if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;
+  // Aim at ~12 row items per compute unit (256 CUs), but keep each at least
+  // 256 keys long so its fixed costs stay small.
+  const int64_t target_items = 256 * 12;
+  int64_t s = (total_row_keys + target_items - 1) / std::max<int64_t>(target_items, 1);
+  s = std::max<int64_t>(s, 256);
+  s = std::min<int64_t>(s, 1 << 20);
+  return static_cast<int32_t>(((s + kBlock - 1) / kBlock) * kBlock);
+}
+
+}  // namespace
+}  // namespace aug
+
+using namespace aug;
+
+extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_desc* b,
+                                    int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
+                                    aug_attn_plan_info* info) {
+  const char* who = "aug_attn_plan";
+  if (aug_status st = check_shape(s, who); st != AUG_OK) return st;
+  if (!b || !info) return fail(AUG_ERR_INVALID, "%s: batch or info is NULL", who);
+  const int32_t n = b->num_reqs;
+  if (n < 0) return fail(AUG_ERR_INVALID, "%s: num_reqs %d < 0", who, n);
+  if (n > 0 && (!b->q_start || !b->ctx_len || !b->bt_start))
+    return fail(AUG_ERR_INVALID, "%s: batch arrays are NULL", who);
+  if (b->num_pool_blocks < 1) return fail(AUG_ERR_INVALID, "%s: empty pool", who);
+  if (n > 0 && b->q_start[0] != 0) return fail(AUG_ERR_INVALID, "%s: q_start[0] != 0", who);
+  const int32_t hkv = s->num_kv_heads;
+  const int32_t g = s->num_q_heads / hkv;
+  int64_t total_row_keys = 0;
+  for (int32_t r = 0; r < n; ++r) {
+    const int64_t q = static_cast<int64_t>(b->q_start[r + 1]) - b->q_start[r];
+    const int64_t ctx = b->ctx_len[r];
+    if (q < 1) return fail(AUG_ERR_INVALID, "%s: request %d has %lld rows", who, r, (long long)q);
+    if (ctx < q)
+      return fail(AUG_ERR_INVALID, "%s: request %d has ctx_len %lld < rows %lld", who, r,
+                  (long long)ctx, (long long)q);
+    const int64_t need = (ctx + kBlock - 1) / kBlock;
+    const int64_t have = static_cast<int64_t>(b->bt_start[r + 1]) - b->bt_start[r];
+    if (b->bt_start[r] < 0 || have < need)
+      return fail(AUG_ERR_INVALID, "%s: request %d lists %lld blocks, needs %lld", who, r,
+                  (long long)have, (long long)need);
+    if (b->block_ids) {
+      for (int64_t i = 0; i < need; ++i) {
+        const int32_t id = b->block_ids[b->bt_start[r] + i];
+        if (id < 0 || id >= b->num_pool_blocks)
+          return fail(AUG_ERR_INVALID, "%s: request %d block %lld is %d, pool has %d", who, r,
+                      (long long)i, id, b->num_pool_blocks);
+      }
+    }
+    const bool tiled = q > 1 && tiles_supported(*s);
+    if (!tiled) {
+      // rows at positions ctx-q .. ctx-1 read pos+1 keys each
+      total_row_keys += (q * (2 * ctx - q + 1) / 2) * hkv;
+    }
+  }
+  const int64_t total_rows = n > 0 ? b->q_start[n] : 0;
+  if (total_rows > (int64_t{1} << 30))
+    return fail(AUG_ERR_UNSUPPORTED, "%s: %lld rows", who, (long long)total_rows);
+
+  const int32_t split = choose_split(total_row_keys, kv_split_tokens);
+  const int32_t pos_per_tile = kTileRows / g;
+
+  // Row items: a request's spans are equal (within one block), so ordering
+  // requests by span length orders their items longest first.
+  struct RowReq {
+    int32_t r, span, nspan;
+  };
+  std::vector<RowReq> row_reqs;
+  std::vector<Sized> tiles;
+  int64_t n_row_items = 0, n_groups = 0, n_parts = 0;
+  int64_t order = 0;
+  for (int32_t r = 0; r < n; ++r) {
+    const int32_t q = b->q_start[r + 1] - b->q_start[r];
+    const int32_t ctx = b->ctx_len[r];
+    if (q > 1 && tiles_supported(*s)) {
+      for (int32_t j0 = 0; j0 < q; j0 += pos_per_tile) {
+        const int32_t nr = std::min(pos_per_tile, q - j0);
+        const int32_t pos0 = ctx - q + j0;
+        for (int32_t h = 0; h < hkv; ++h) {
+          WorkItem it{};
+          it.kind_kvh = h | (kTileItem << 16);
+          it.q_row0 = b->q_start[r] + j0;
+          it.n_rows = nr;
+          it.key_begin = 0;
+          it.key_end = pos0 + nr;
+          it.pos0 = pos0;
+          it.bt_off = b->bt_start[r];
+          it.part = -1;
+          tiles.push_back({it, static_cast<int64_t>(nr) * it.key_end, order++});   // work ~ rows x keys
+        }
+      }
+      continue;
+    }
+    // decodes have one row; rows of an untiled prefill get spans of their own length
+    const int32_t keys = ctx;  // the longest row of the request
+    const int32_t nspan = (keys + split - 1) / split;
+    int32_t span = (keys + nspan - 1) / nspan;
+    span = ((span + kBlock - 1) / kBlock) * kBlock;
+    row_reqs.push_back({r, span, (keys + span - 1) / span});
+    for (int32_t j = 0; j < q; ++j) {
+      const int32_t k = ctx - q + j + 1;
+      const int64_t ns = (k + span - 1) / span;
+      n_row_items += ns * hkv;
+      if (ns > 1) {
+        n_groups += hkv;
+        n_parts += ns * hkv;
+      }
+    }
+  }
+  std::sort(tiles.begin(), tiles.end(), [](const Sized& a, const Sized& c) {
+    if (a.weight != c.weight) return a.weight > c.weight;
+    return a.order < c.order;
+  });
+  std::stable_sort(row_reqs.begin(), row_reqs.end(),
+                   [](const RowReq& a, const RowReq& c) { return a.span > c.span; });
+  (void)order;
+
+  const int64_t n_items = static_cast<int64_t>(tiles.size()) + n_row_items;
+  if (n_items > (int64_t{1} << 30))
+    return fail(AUG_ERR_UNSUPPORTED, "%s: %lld work items", who, (long long)n_items);
+  const int64_t items_off = sizeof(PlanHeader);
+  const int64_t groups_off = items_off + n_items * static_cast<int64_t>(sizeof(WorkItem));
+  if (n_parts > (int64_t{1} << 30))
+    return fail(AUG_ERR_UNSUPPORTED, "%s: %lld split-K partials", who, (long long)n_parts);
+  const int64_t plan_bytes = groups_off + n_groups * static_cast<int64_t>(sizeof(MergeGroup));
+  const int64_t ws = ((n_parts * partial_floats(g, s->head_dim) * 4 + 255) / 256) * 256;
+
+  std::memset(info, 0, sizeof(*info));
+  info->plan_bytes = plan_bytes;
+  info->workspace_bytes = ws;
+  info->num_items = static_cast<int32_t>(n_items);
+  info->num_prefill_items = static_cast<int32_t>(tiles.size());
+  info->num_merge_groups = static_cast<int32_t>(n_groups);
+  info->num_partials = static_cast<int32_t>(n_parts);
+  info->kv_split_tokens = split;
+  info->total_rows = static_cast<int32_t>(total_rows);
+  info->num_reqs = n;
+  if (!plan_host) return AUG_OK;
+  if (plan_cap < static_cast<size_t>(plan_bytes))
+    return fail(AUG_ERR_NO_SPACE, "%s: plan buffer %zu < %lld bytes", who, plan_cap,
+                (long long)plan_bytes);
+
+  auto* base = static_cast<unsigned char*>(plan_host);
+  PlanHeader hdr{};
+  hdr.magic = kPlanMagic;
+  hdr.version = kPlanVersion;
+  hdr.num_items = info->num_items;
+  hdr.num_tile_items = info->num_prefill_items;
+  hdr.num_groups = info->num_merge_groups;
+  hdr.num_partials = info->num_partials;
+  hdr.kv_split = split;
+  hdr.total_rows = info->total_rows;
+  hdr.items_offset = static_cast<int32_t>(items_off);
+  hdr.groups_offset = static_cast<int32_t>(groups_off);
+  std::memcpy(base, &hdr, sizeof(hdr));
+  auto* items = reinterpret_cast<WorkItem*>(base + items_off);
+  auto* groups = reinterpret_cast<MergeGroup*>(base + groups_off);
+  size_t k = 0;
+  for (const Sized& t : tiles) items[k++] = t.item;
+  int32_t parts = 0, ng = 0;
+  for (const RowReq& rr : row_reqs) {
+    const int32_t r = rr.r;
+    const int32_t q = b->q_start[r + 1] - b->q_start[r];
+    const int32_t ctx = b->ctx_len[r];
+    for (int32_t j = 0; j < q; ++j) {
+      const int32_t pos = ctx - q + j;
+      const int32_t keys = pos + 1;
+      const int32_t nspan = (keys + rr.span - 1) / rr.span;
+      for (int32_t h = 0; h < hkv; ++h) {
+        const int32_t part0 = nspan > 1 ? parts : -1;
+        if (nspan > 1) {
+          groups[ng++] = MergeGroup{b->q_start[r] + j, h, part0, nspan};
+          parts += nspan;
+        }
+        for (int32_t sidx = 0; sidx < nspan; ++sidx) {
+          WorkItem it{};
+          it.kind_kvh = h | (kRowItem << 16);
+          it.q_row0 = b->q_start[r] + j;
+          it.n_rows = 1;
+          it.key_begin = sidx * rr.span;
+          it.key_end = std::min(keys, (sidx + 1) * rr.span);
+          it.pos0 = pos;
+          it.bt_off = b->bt_start[r];
+          it.part = nspan > 1 ? part0 + sidx : -1;
+          items[k++] = it;
+        }
+      }
+    }
+  }
+  return AUG_OK;
+}

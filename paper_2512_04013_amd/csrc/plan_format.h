@@ -1,0 +1,62 @@
+// Work-list ("plan image") of one attention launch, written by the host
+// planner and read by the kernels. Plain data, position independent.
+#pragma once
+
+#include <cstdint>
+
+namespace aug {
+
+constexpr int32_t kPlanMagic = 0x4E4C5041;  // "APLN"
+constexpr int32_t kPlanVersion = 1;
+constexpr int32_t kBlock = 16;              // tokens per KV block
+constexpr int32_t kKeyTile = 64;            // keys per MFMA tile (4 blocks)
+constexpr int32_t kTileRows = 128;          // query rows (positions x group heads) per MFMA tile
+
+enum ItemKind : int32_t {
+  kRowItem = 0,   // one query row (all heads of one KV head group) against a key span, VALU
+  kTileItem = 1,  // a tile of consecutive query rows of one chunk, causal, MFMA
+};
+
+struct PlanHeader {          // 64 bytes
+  int32_t magic;
+  int32_t version;
+  int32_t num_items;
+  int32_t num_tile_items;
+  int32_t num_groups;
+  int32_t num_partials;
+  int32_t kv_split;
+  int32_t total_rows;
+  int32_t items_offset;      // bytes from the start of the image
+  int32_t groups_offset;
+  int32_t reserved[6];
+};
+
+struct WorkItem {            // 32 bytes
+  int32_t kind_kvh;          // KV head | kind << 16
+  int32_t q_row0;            // first global row of Q/O
+  int32_t n_rows;            // rows (context positions) in the item
+  int32_t key_begin;         // first key (multiple of kBlock)
+  int32_t key_end;           // one past the last key any row reads
+  int32_t pos0;              // context position of the first row
+  int32_t bt_off;            // offset of the request's block table in block_ids
+  int32_t part;              // row items: partial slot, -1 = write O directly
+};
+
+struct MergeGroup {          // 16 bytes
+  int32_t q_row;
+  int32_t kvh;
+  int32_t part0;
+  int32_t n_parts;
+};
+
+static_assert(sizeof(PlanHeader) == 64, "plan header layout");
+static_assert(sizeof(WorkItem) == 32, "work item layout");
+static_assert(sizeof(MergeGroup) == 16, "merge group layout");
+
+// Split-K partial of one (row, KV head, key span): unnormalised o[G][D]
+// relative to the running maximum, then m[G] (log2 domain) and l[G].
+constexpr int64_t partial_floats(int32_t group, int32_t head_dim) {
+  return static_cast<int64_t>(group) * (head_dim + 2);
+}
+
+}  // namespace aug

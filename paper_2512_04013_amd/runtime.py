@@ -1,0 +1,104 @@
+"""Device-side plumbing around the C ABI: torch tensors for the pool, the
+plan image and the workspace, and one call per step of the hot path.
+
+Everything here is argument marshalling and memory management (torch owns
+the device memory and the stream); the arithmetic runs in libaug.so.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import (aug_attn_mixed, aug_attn_plan, aug_kv_park, aug_kv_record_bytes, aug_kv_resume,
+               make_shape)
+
+_TORCH_STORAGE = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.uint8}
+
+
+def to_device_array(x: np.ndarray, dtype: str, device) -> torch.Tensor:
+    """Host bit patterns (float32 / uint16 bf16 / uint8 fp8) -> device tensor."""
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(device)
+    if dtype == "fp8":
+        return torch.from_numpy(np.ascontiguousarray(x, dtype=np.uint8)).to(device)
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(device)
+
+
+def to_host_f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+class PagedKV:
+    """A KV pool on the device plus its park/resume staging."""
+
+    def __init__(self, shape, k_cache, v_cache, k_scale=None, v_scale=None, staging_bytes=1 << 28):
+        self.shape = shape
+        self.k_cache, self.v_cache = k_cache, v_cache
+        self.k_scale, self.v_scale = k_scale, v_scale
+        self.num_pool_blocks = int(k_cache.shape[0])
+        self.record_bytes = aug_kv_record_bytes(shape)
+        staging_bytes = max(self.record_bytes, (staging_bytes // self.record_bytes) * self.record_bytes)
+        self.staging = torch.empty(staging_bytes, dtype=torch.uint8, device=k_cache.device)
+
+    def host_buffer(self, n_blocks: int) -> torch.Tensor:
+        return torch.empty(max(1, n_blocks * self.record_bytes), dtype=torch.uint8, pin_memory=True)
+
+    def park(self, blocks_host: np.ndarray, blocks_dev: torch.Tensor, host_dst: torch.Tensor, stream=None):
+        aug_kv_park(self.shape, self.k_cache, self.v_cache, self.k_scale, self.v_scale, blocks_dev,
+                    len(blocks_host), self.num_pool_blocks, host_dst, self.staging,
+                    block_ids_host=blocks_host, stream=stream)
+
+    def resume(self, blocks_host: np.ndarray, blocks_dev: torch.Tensor, host_src: torch.Tensor, stream=None):
+        aug_kv_resume(self.shape, self.k_cache, self.v_cache, self.k_scale, self.v_scale, blocks_dev,
+                      len(blocks_host), self.num_pool_blocks, host_src, self.staging,
+                      block_ids_host=blocks_host, stream=stream)
+
+
+class MixedAttention:
+    """One planned mixed batch: its plan image and workspace on the device,
+    its output tensor, and the launch."""
+
+    def __init__(self, shape, kv: PagedKV, q_start, ctx_len, bt_start, block_ids_host,
+                 block_ids_dev: torch.Tensor, kv_split_tokens: int = 0, check_blocks: bool = True):
+        self.shape, self.kv = shape, kv
+        device = kv.k_cache.device
+        self.info, plan = aug_attn_plan(shape, q_start, ctx_len, bt_start, kv.num_pool_blocks,
+                                        block_ids_host if check_blocks else None,
+                                        kv_split_tokens=kv_split_tokens)
+        self.plan_host = torch.from_numpy(plan.copy()).pin_memory()
+        self.plan_dev = torch.empty(max(1, plan.size), dtype=torch.uint8, device=device)
+        self.plan_dev[:plan.size].copy_(self.plan_host, non_blocking=True)
+        self.workspace = torch.empty(max(256, int(self.info.workspace_bytes)), dtype=torch.uint8,
+                                     device=device)
+        self.block_ids = block_ids_dev
+        rows = int(self.info.total_rows)
+        out_dtype = torch.float32 if shape.out_dtype == 0 else torch.bfloat16
+        self.out = torch.empty((rows, shape.num_q_heads, shape.head_dim), dtype=out_dtype, device=device)
+
+    def run(self, q: torch.Tensor, stream=None):
+        aug_attn_mixed(self.shape, self.info, self.plan_dev, q, self.kv.k_cache, self.kv.v_cache,
+                       self.kv.k_scale, self.kv.v_scale, self.block_ids, self.kv.num_pool_blocks,
+                       self.out, self.workspace, stream=stream)
+        return self.out
+
+
+def shape_of(batch) -> object:
+    return make_shape(batch.num_q_heads, batch.num_kv_heads, batch.head_dim, batch.q_dtype,
+                      batch.kv_dtype, batch.out_dtype, batch.softmax_scale)
+
+
+def upload_batch(batch, device="cuda", staging_bytes=1 << 28):
+    """Move a host batch (fields as produced by the seeded generators) to the
+    device: returns (shape, PagedKV, q tensor, block_ids tensor)."""
+    shape = shape_of(batch)
+    k = to_device_array(batch.k_cache, batch.kv_dtype, device)
+    v = to_device_array(batch.v_cache, batch.kv_dtype, device)
+    ks = vs = None
+    if batch.kv_dtype == "fp8":
+        ks = torch.from_numpy(batch.k_scale).to(device)
+        vs = torch.from_numpy(batch.v_scale).to(device)
+    kv = PagedKV(shape, k, v, ks, vs, staging_bytes=staging_bytes)
+    q = to_device_array(batch.q, batch.q_dtype, device)
+    bids = torch.from_numpy(np.ascontiguousarray(batch.block_ids, dtype=np.int32)).to(device)
+    return shape, kv, q, bids

@@ -25,7 +25,9 @@ budget with parked and resumed requests, a long-context decode batch, and the
 
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
+import os
 from typing import List, Optional, Sequence
 
 import numpy as np
@@ -101,9 +103,9 @@ class AttnBatch:
 
 def round_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """float32 -> bf16 bit patterns, round to nearest even (finite inputs)."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+    u = np.array(x, dtype=np.float32, copy=True).view(np.uint32)
+    u += ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    return np.ascontiguousarray(u.view(np.uint16)[..., 1::2])
 
 
 def encode_e4m3fn_bits(y: np.ndarray) -> np.ndarray:
@@ -154,23 +156,32 @@ def _to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def _write_tokens(pool, scale, vals, blocks, ctx, kv_dtype):
-    """Write ``vals`` [ctx, H_kv, D] (float32) into ``pool`` at ``blocks``."""
+    """Write ``vals`` [ctx, H_kv, D] (float32) into ``pool`` at ``blocks``; the
+    slots past ``ctx`` in the last block keep their NaN poison."""
     nblk = -(-ctx // BLOCK)
-    t = np.arange(ctx)
-    blk = blocks[t // BLOCK]
-    slot = t % BLOCK
+    h_kv, d = vals.shape[1], vals.shape[2]
+    blocks = np.asarray(blocks[:nblk], dtype=np.int64)
+    full = ctx // BLOCK
     if kv_dtype == "fp8":
-        h_kv, d = vals.shape[1], vals.shape[2]
         pad = np.zeros((nblk * BLOCK, h_kv, d), dtype=np.float32)
         pad[:ctx] = vals
         per_block = pad.reshape(nblk, BLOCK, h_kv, d)
         amax = np.abs(per_block).max(axis=(1, 3))               # [nblk, H_kv]
         s = np.where(amax > 0, amax / 448.0, 1.0).astype(np.float32)
-        scale[blocks[:nblk]] = s
-        s_tok = s[t // BLOCK]                                    # [ctx, H_kv]
-        pool[blk, :, slot, :] = encode_e4m3fn_bits(vals / s_tok[:, :, None])
-    else:
-        pool[blk, :, slot, :] = _to_storage(vals, kv_dtype)
+        scale[blocks] = s
+        codes = encode_e4m3fn_bits(per_block / s[:, None, :, None]).transpose(0, 2, 1, 3)
+        if full:
+            pool[blocks[:full]] = codes[:full]
+        tail = ctx - full * BLOCK
+        if tail:
+            pool[blocks[full], :, :tail, :] = codes[full, :, :tail, :]
+        return
+    stored = _to_storage(vals, kv_dtype)
+    if full:
+        pool[blocks[:full]] = stored[:full * BLOCK].reshape(full, BLOCK, h_kv, d).transpose(0, 2, 1, 3)
+    tail = ctx - full * BLOCK
+    if tail:
+        pool[blocks[full], :, :tail, :] = stored[full * BLOCK:].transpose(1, 0, 2)
 
 
 def make_batch_from_lengths(
@@ -241,20 +252,27 @@ def make_batch_from_lengths(
     else:
         k_scale = v_scale = None
 
+    # every request (and every paused extra request) draws from its own stream,
+    # so the bytes do not depend on how the work is spread over threads
     kv_std32 = np.float32(kv_std)
-    for r in range(n_req):
-        ctx = int(ctx_lens[r])
-        kf = rng.standard_normal((ctx, num_kv_heads, head_dim), dtype=np.float32) * kv_std32
-        vf = rng.standard_normal((ctx, num_kv_heads, head_dim), dtype=np.float32) * kv_std32
-        where = src_tables.get(r, tables[r])
-        _write_tokens(k_cache, k_scale, kf, where, ctx, kv_dtype)
-        _write_tokens(v_cache, v_scale, vf, where, ctx, kv_dtype)
-    for e in range(len(extra)):
-        ctx = int(extra[e])
-        kf = rng.standard_normal((ctx, num_kv_heads, head_dim), dtype=np.float32) * kv_std32
-        vf = rng.standard_normal((ctx, num_kv_heads, head_dim), dtype=np.float32) * kv_std32
-        _write_tokens(k_cache, k_scale, kf, extra_tables[e], ctx, kv_dtype)
-        _write_tokens(v_cache, v_scale, vf, extra_tables[e], ctx, kv_dtype)
+    jobs = [(r, int(ctx_lens[r]), src_tables.get(r, tables[r])) for r in range(n_req)]
+    jobs += [(n_req + e, int(extra[e]), extra_tables[e]) for e in range(len(extra))]
+
+    def fill(job):
+        key, ctx, where = job
+        g = np.random.default_rng([seed, 7, key])
+        for cache, scale in ((k_cache, k_scale), (v_cache, v_scale)):
+            x = g.standard_normal((ctx, num_kv_heads, head_dim), dtype=np.float32)
+            x *= kv_std32
+            _write_tokens(cache, scale, x, where, ctx, kv_dtype)
+
+    workers = min(16, os.cpu_count() or 1)
+    if workers > 1 and len(jobs) > 1:
+        with cf.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(fill, jobs))
+    else:
+        for j in jobs:
+            fill(j)
 
     q_start = np.zeros(n_req + 1, dtype=np.int32)
     q_start[1:] = np.cumsum(q_lens)

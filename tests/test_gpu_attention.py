@@ -1,0 +1,192 @@
+"""GPU parity of aug_attn_mixed against the oracle (through the C ABI)."""
+
+import copy
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+import synth  # noqa: E402
+from oracle import attention as oa  # noqa: E402
+from oracle import kvpark  # noqa: E402
+from synth.attn_inputs import make_batch_from_lengths  # noqa: E402
+from tests.gpu_util import compare, rows_of, say  # noqa: E402
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def _run(batch, kv_split=0, staging_bytes=1 << 26):
+    from paper_2512_04013_amd import runtime as rt
+    shape, kv, q, bids = rt.upload_batch(batch, staging_bytes=staging_bytes)
+    att = rt.MixedAttention(shape, kv, batch.q_start, batch.ctx_len, batch.bt_start, batch.block_ids,
+                            bids, kv_split_tokens=kv_split)
+    out = att.run(q)
+    torch.cuda.synchronize()
+    return rt.to_host_f64(out), att
+
+
+# ---- tiny fp32 mixed batch: every row, several splits ------------------------------------
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("split", [0, 32, 64])
+def test_tiny_mixed_fp32(seed, split):
+    b = synth.make_tiny_mixed(seed=seed)
+    say(f"[tiny-mixed fp32] seed={seed} split={split}")
+    got, att = _run(b, kv_split=split)
+    want = oa.attention_for(b)
+    compare(got, want, "f32", what=f"tiny seed={seed} split={split} parts={att.info.num_partials}")
+
+
+# ---- ragged shapes across group sizes, head dims and dtypes ---------------------------------
+
+CASES = [
+    # (q_lens, ctx_lens, hq, hkv, d, q/kv dtype)
+    ([1, 1, 1, 5, 1, 40], [1, 17, 300, 5, 16, 333], 8, 8, 64, "bf16"),        # G=1, ctx=1, q=ctx
+    ([1, 70, 1, 3], [200, 70, 1000, 29], 8, 4, 128, "bf16"),                 # G=2
+    ([33, 1, 129, 1], [100, 1, 500, 2049], 32, 8, 128, "bf16"),              # G=4, >1 tile
+    ([17, 1, 1, 16], [17, 64, 65, 600], 64, 8, 128, "bf16"),                 # G=8
+    ([1, 9, 1], [513, 100, 48], 16, 4, 64, "bf16"),                          # D=64 tiles
+    ([1, 3, 1, 1], [400, 40, 1, 77], 64, 8, 128, "fp8"),                     # fp8 KV (row path)
+    ([2, 1, 1], [35, 250, 16], 8, 2, 128, "f32"),                            # f32 D=128, G=4
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+@pytest.mark.parametrize("sharp", [False, True])
+def test_ragged_shapes(case, sharp):
+    q_lens, ctx_lens, hq, hkv, d, dt = CASES[case]
+    qd = "f32" if dt == "f32" else "bf16"
+    b = make_batch_from_lengths(f"case{case}", q_lens, ctx_lens, num_q_heads=hq, num_kv_heads=hkv,
+                                head_dim=d, q_dtype=qd, kv_dtype=dt, out_dtype=qd,
+                                n_pool_blocks=512, seed=100 + case,
+                                kv_std=1.0 if sharp else 1.0 / np.sqrt(d))
+    say(f"[ragged] case={case} sharp={sharp} G={hq // hkv} D={d} kv={dt}")
+    for split in (0, 48):
+        got, att = _run(b, kv_split=split)
+        want = oa.attention_for(b)
+        compare(got, want, qd, what=f"case{case} sharp={sharp} split={split} tiles={att.info.num_prefill_items}")
+
+
+# ---- the 8B-shaped decode batch at full size ----------------------------------------------------
+
+@pytest.fixture(scope="module")
+def decode_8b():
+    return synth.make_decode_8b(seed=0)
+
+
+@pytest.mark.parametrize("split", [0, 128, 1024])
+def test_decode_8b_full(decode_8b, split):
+    b = decode_8b
+    say(f"[decode-8b] 256 decodes, split={split}")
+    got, att = _run(b, kv_split=split)
+    want = oa.attention_for(b)
+    compare(got, want, "bf16", what=f"decode-8b split={split} items={att.info.num_items}")
+
+
+def test_decode_8b_sharp_full():
+    b = synth.make_decode_8b(seed=1, sharp=True)
+    say("[decode-8b sharp] 256 decodes")
+    got, _ = _run(b)
+    compare(got, oa.attention_for(b), "bf16", what="decode-8b sharp")
+
+
+def test_block_permutation_gives_identical_bits(decode_8b):
+    b = synth.make_decode_8b(seed=5, n_req=48, n_pool_blocks=8192)
+    say("[permutation] 48 decodes")
+    got, _ = _run(b)
+    perm = np.random.default_rng(9).permutation(b.num_pool_blocks)
+    b2 = copy.copy(b)
+    b2.k_cache = np.empty_like(b.k_cache)
+    b2.v_cache = np.empty_like(b.v_cache)
+    b2.k_cache[perm] = b.k_cache
+    b2.v_cache[perm] = b.v_cache
+    b2.block_ids = perm[b.block_ids].astype(np.int32)
+    got2, _ = _run(b2)
+    assert np.array_equal(got.view(np.uint64), got2.view(np.uint64))
+
+
+def test_results_do_not_depend_on_the_split_beyond_tolerance(decode_8b):
+    b = synth.make_decode_8b(seed=6, n_req=32, n_pool_blocks=8192, sharp=True)
+    say("[split independence] 32 decodes")
+    outs = [_run(b, kv_split=s)[0] for s in (16, 64, 256, 4096)]
+    for o in outs[1:]:
+        assert np.abs(o - outs[0]).max() <= 1e-2
+
+
+# ---- the mixed batch: resume parked requests, then attention ----------------------------------
+
+def _park_resume_then_attend(b, split=0, staging_bytes=1 << 26, sample=None):
+    from paper_2512_04013_amd import runtime as rt
+    shape, kv, q, bids = rt.upload_batch(b, staging_bytes=staging_bytes)
+    pk = b.park
+    dev = kv.k_cache.device
+    src = torch.from_numpy(pk.resume_src_blocks).to(dev)
+    dst = torch.from_numpy(pk.resume_blocks).to(dev)
+    host = kv.host_buffer(len(pk.resume_src_blocks))
+    kv.park(pk.resume_src_blocks, src, host)
+    torch.cuda.synchronize()
+    image = host.numpy()[:len(pk.resume_src_blocks) * kv.record_bytes]
+    want_img = kvpark.park(b.k_cache, b.v_cache, b.k_scale, b.v_scale, b.kv_dtype, pk.resume_src_blocks)
+    assert np.array_equal(image, want_img), "parked image differs from the oracle's"
+    # the source blocks are free now: poison them, then resume into the new blocks
+    kv.k_cache.view(torch.uint8)[src.long()] = 0xFF
+    kv.v_cache.view(torch.uint8)[src.long()] = 0xFF
+    kv.resume(pk.resume_blocks, dst, host)
+    att = rt.MixedAttention(shape, kv, b.q_start, b.ctx_len, b.bt_start, b.block_ids, bids,
+                            kv_split_tokens=split)
+    out = att.run(q)
+    parked_others = None
+    if len(pk.park_blocks):
+        pb = torch.from_numpy(pk.park_blocks).to(dev)
+        parked_others = kv.host_buffer(len(pk.park_blocks))
+        kv.park(pk.park_blocks, pb, parked_others)
+    torch.cuda.synchronize()
+    k_res, v_res, _, _ = kvpark.resume(b.k_cache, b.v_cache, b.k_scale, b.v_scale, b.kv_dtype,
+                                       pk.resume_blocks, want_img)
+    if parked_others is not None:
+        want_other = kvpark.park(b.k_cache, b.v_cache, b.k_scale, b.v_scale, b.kv_dtype, pk.park_blocks)
+        assert np.array_equal(parked_others.numpy()[:want_other.size], want_other)
+    # resumed blocks hold exactly the parked bytes
+    rb = torch.from_numpy(pk.resume_blocks).long().to(dev)
+    dev_k = kv.k_cache.view(torch.uint8)[rb].cpu().numpy() if b.kv_dtype == "fp8" else \
+        kv.k_cache[rb].view(torch.int16 if b.kv_dtype == "bf16" else torch.int32).cpu().numpy()
+    host_k = b.k_cache[pk.resume_src_blocks]
+    assert np.array_equal(dev_k.view(np.uint8), np.ascontiguousarray(host_k).view(np.uint8))
+    return rt.to_host_f64(out), att, (k_res, v_res)
+
+
+def test_mixed_8b_small_all_rows():
+    b = synth.make_mixed_8b(seed=3, n_dec=64, n_pre=2, n_pool_blocks=16384)
+    say("[mixed-8b small] 2 prefill chunks + 64 decodes, resume 30%")
+    got, att, (k_res, v_res) = _park_resume_then_attend(b)
+    assert att.info.num_prefill_items > 0
+    want = oa.attention_for(b, k_cache=k_res, v_cache=v_res)
+    compare(got, want, "bf16", what="mixed-8b small")
+
+
+def test_mixed_8b_full_size_sampled():
+    b = synth.make_mixed_8b(seed=0)
+    say(f"[mixed-8b full] {b.num_reqs} requests, {b.total_q} rows, resume {len(b.park.resume_blocks)} blocks")
+    got, att, (k_res, v_res) = _park_resume_then_attend(b, staging_bytes=1 << 27)
+    rng = np.random.default_rng(0)
+    dec = rng.choice(np.arange(3, b.num_reqs), size=48, replace=False)
+    reqs = [0] + sorted(int(r) for r in dec)
+    want = oa.attention_for(b, requests=reqs, k_cache=k_res, v_cache=v_res)
+    rows = rows_of(b, reqs)
+    compare(got, want, "bf16", rows=rows, what="mixed-8b full (1 prefill chunk + 48 decodes)")
+    assert np.isfinite(got).all()
+
+
+def test_long_context_sampled():
+    b = synth.make_long_context(seed=0)
+    say(f"[long-context] 64 decodes 16k-32k, resume 8, park 8 ({len(b.park.park_blocks)} blocks)")
+    got, att, (k_res, v_res) = _park_resume_then_attend(b, staging_bytes=1 << 28)
+    assert att.info.num_merge_groups > 0
+    resumed = [r for r in range(b.num_reqs)
+               if set(b.blocks_of(r).tolist()) & set(b.park.resume_blocks[:1].tolist())]
+    reqs = sorted(set([0, 1, 63] + resumed[:1] + list(np.random.default_rng(1).choice(64, 4, replace=False))))
+    want = oa.attention_for(b, requests=reqs, k_cache=k_res, v_cache=v_res)
+    compare(got, want, "bf16", rows=rows_of(b, reqs), what=f"long-context reqs={reqs}")
+    assert np.isfinite(got).all()

@@ -1,0 +1,263 @@
+"""CPU tests of the C ABI library: it loads without a GPU, exports every
+symbol include/aug.h declares, the planner validates batches and covers every
+key of every row exactly once, and the C++ batch former equals the oracle
+former bit for bit. No device call is made here."""
+
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2512_04013_amd as aug
+from paper_2512_04013_amd import AugError
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.skipif(not os.path.exists(aug.LIB_PATH), reason="libaug.so not built")
+
+
+def test_library_exports_every_declared_symbol():
+    header = open(os.path.join(ROOT, "include", "aug.h")).read()
+    declared = set(re.findall(r"\b(aug_[a-z_]+)\s*\(", header))
+    assert declared == set(aug.EXPORTED)
+    L = aug.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+    assert aug.aug_abi_version() >> 16 == 1
+    assert aug.aug_status_string(aug.AUG_ERR_NO_SPACE) == "AUG_ERR_NO_SPACE"
+
+
+def _shape(b):
+    return aug.make_shape(b.num_q_heads, b.num_kv_heads, b.head_dim, b.q_dtype, b.kv_dtype,
+                          b.out_dtype, b.softmax_scale)
+
+
+def _decode_plan(plan):
+    hdr = plan[:64].view(np.int32)
+    assert hdr[0] == 0x4E4C5041 and hdr[1] == 1
+    n_items, n_groups = hdr[2], hdr[4]
+    items = plan[hdr[8]:hdr[8] + 32 * n_items].view(np.int32).reshape(-1, 8)
+    groups = plan[hdr[9]:hdr[9] + 16 * n_groups].view(np.int32).reshape(-1, 4)
+    return hdr, items, groups
+
+
+@pytest.mark.parametrize("cfg", [1, 3])
+@pytest.mark.parametrize("split", [0, 32, 256])
+def test_plan_covers_every_key_of_every_row_once(cfg, split):
+    if cfg == 3:
+        b = synth.make_mixed_8b(seed=1, n_dec=40, n_pre=2, n_pool_blocks=8192)
+    else:
+        b = synth.make_tiny_mixed(seed=3)
+    info, plan = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
+                                   b.block_ids, kv_split_tokens=split)
+    hdr, items, groups = _decode_plan(plan)
+    assert info.num_items == len(items) and info.num_merge_groups == len(groups)
+    g = b.num_q_heads // b.num_kv_heads
+    tiled = b.q_dtype == "bf16" and b.kv_dtype == "bf16"
+    cover = {}
+    parts_seen = set()
+    for kind_kvh, q_row0, n_rows, kb, ke, pos0, bt_off, part in items:
+        kind, kvh = kind_kvh >> 16, kind_kvh & 0xFFFF
+        r = int(np.searchsorted(b.q_start, q_row0, side="right") - 1)
+        assert bt_off == b.bt_start[r]
+        q_len = b.q_start[r + 1] - b.q_start[r]
+        if kind == 1:
+            assert tiled and q_len > 1 and kb == 0 and part == -1
+            assert n_rows <= 128 // g
+            for j in range(n_rows):
+                row = q_row0 + j
+                pos = b.ctx_len[r] - q_len + (row - b.q_start[r])
+                assert pos0 + j == pos and ke >= pos + 1
+                cover.setdefault((row, kvh), []).append((0, pos + 1))
+        else:
+            assert n_rows == 1 and kb % 16 == 0
+            pos = b.ctx_len[r] - q_len + (q_row0 - b.q_start[r])
+            assert pos0 == pos and ke <= pos + 1
+            cover.setdefault((q_row0, kvh), []).append((kb, ke))
+            if part >= 0:
+                assert part not in parts_seen
+                parts_seen.add(part)
+    for r in range(b.num_reqs):
+        for row in range(b.q_start[r], b.q_start[r + 1]):
+            pos = b.ctx_len[r] - (b.q_start[r + 1] - b.q_start[r]) + (row - b.q_start[r])
+            for h in range(b.num_kv_heads):
+                spans = sorted(cover[(row, h)])
+                assert spans[0][0] == 0 and spans[-1][1] == pos + 1
+                assert all(a[1] == c[0] for a, c in zip(spans, spans[1:]))
+    assert parts_seen == set(range(info.num_partials))
+    for q_row, kvh, part0, n in groups:
+        assert n > 1 and len(cover[(q_row, kvh)]) == n
+
+
+def test_plan_rejects_invalid_batches():
+    b = synth.make_tiny_mixed(seed=0)
+    s = _shape(b)
+
+    def plan(**kw):
+        args = dict(q_start=b.q_start, ctx_len=b.ctx_len, bt_start=b.bt_start,
+                    num_pool_blocks=b.num_pool_blocks, block_ids=b.block_ids)
+        args.update(kw)
+        return aug.aug_attn_plan(s, **args)
+
+    plan()
+    bad_ctx = b.ctx_len.copy()
+    bad_ctx[np.argmax(b.q_len > 1)] = 5           # fewer keys than rows
+    with pytest.raises(AugError) as e:
+        plan(ctx_len=bad_ctx)
+    assert e.value.status == aug.AUG_ERR_INVALID
+    bad_ids = b.block_ids.copy()
+    bad_ids[3] = b.num_pool_blocks
+    with pytest.raises(AugError):
+        plan(block_ids=bad_ids)
+    plan(block_ids=None, num_pool_blocks=b.num_pool_blocks)    # unchecked table is accepted
+    bad_bt = b.bt_start.copy()
+    bad_bt[1:] -= 1                                # first request one block short
+    with pytest.raises(AugError):
+        plan(bt_start=bad_bt)
+    bad_q = b.q_start.copy()
+    bad_q[2] = bad_q[1]                            # an empty request
+    with pytest.raises(AugError):
+        plan(q_start=bad_q)
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_plan(aug.make_shape(4, 4, 96, "f32", "f32", "f32", 0.1), b.q_start, b.ctx_len,
+                          b.bt_start, b.num_pool_blocks)
+    assert e.value.status == aug.AUG_ERR_UNSUPPORTED
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_plan(aug.make_shape(6, 4, 64, "f32", "f32", "f32", 0.1), b.q_start, b.ctx_len,
+                          b.bt_start, b.num_pool_blocks)
+    assert e.value.status == aug.AUG_ERR_INVALID
+    info, p = aug.aug_attn_plan(s, np.zeros(1, np.int32), np.zeros(0, np.int32),
+                                np.zeros(1, np.int32), 8)
+    assert info.num_items == 0
+
+
+def test_park_and_attention_reject_bad_arguments_without_touching_the_gpu():
+    s = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)
+    assert aug.aug_kv_record_bytes(s) == 2 * 8 * 16 * 128 * 2
+    s8 = aug.make_shape(64, 8, 128, "bf16", "fp8", "bf16", 0.088)
+    assert aug.aug_kv_record_bytes(s8) == 2 * 8 * 16 * 128 + 2 * 8 * 4
+    L = aug.lib()
+    ids = np.array([0, 5, 99], np.int32)
+    # id 99 is outside a 50-block pool: refused on the host before any launch
+    st = L.aug_kv_park(aug.C.byref(s), 8, 8, None, None, 8, ids.ctypes.data, 3, 50, 8, 1 << 30, 8,
+                       1 << 20, None)
+    assert st == aug.AUG_ERR_INVALID and "outside" in aug.aug_last_error()
+    st = L.aug_kv_park(aug.C.byref(s), 8, 8, None, None, 8, None, 3, 50, 8, 100, 8, 1 << 20, None)
+    assert st == aug.AUG_ERR_NO_SPACE
+    st = L.aug_kv_resume(aug.C.byref(s8), 8, 8, None, None, 8, None, 3, 50, 8, 1 << 30, 8, 1 << 20, None)
+    assert st == aug.AUG_ERR_INVALID             # fp8 without scales
+    assert L.aug_kv_park(aug.C.byref(s), None, None, None, None, None, None, 0, 50, None, 0, None, 0,
+                         None) == aug.AUG_OK     # nothing to do
+    b = synth.make_tiny_mixed(seed=0)
+    info, _ = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks)
+    if info.num_partials == 0:
+        info, _ = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
+                                    kv_split_tokens=32)
+    assert info.num_partials > 0
+    st = L.aug_attn_mixed(aug.C.byref(_shape(b)), aug.C.byref(info), 8, 8, 8, 8, None, None, 8,
+                          b.num_pool_blocks, 8, None, 0, None)
+    assert st == aug.AUG_ERR_NO_SPACE
+    st = L.aug_attn_mixed(aug.C.byref(_shape(b)), aug.C.byref(info), None, 8, 8, 8, None, None, 8,
+                          b.num_pool_blocks, 8, 8, 1 << 30, None)
+    assert st == aug.AUG_ERR_INVALID
+
+
+# ---- the former, bit-exact against the oracle --------------------------------------------
+
+from oracle import former as of  # noqa: E402
+
+
+def _to_c(reqs):
+    arr = np.zeros(len(reqs), aug.REQUEST_DTYPE)
+    for i, r in enumerate(reqs):
+        for f in ("id", "arrival", "last_sched", "pred_call", "pause_start", "state", "seg",
+                  "prev_policy", "cur_policy", "seg_ctx", "seg_prefill", "pred_out",
+                  "has_next_call", "ctx_len", "pending", "blocks_on_gpu"):
+            arr[i][f] = getattr(r, f)
+    return arr
+
+
+def _c_params(p: of.Params, block_size=16):
+    return aug.former_params(beta=p.beta, t_max=p.t_max, beta_low=p.beta_low, beta_high=p.beta_high,
+                             chunk_cap=p.chunk_cap, t_iter=p.t_iter, fwd_a=p.fwd_a, fwd_b=p.fwd_b,
+                             swap_s_per_tok=p.swap_s_per_tok, n_fwd_max=p.n_fwd_max,
+                             skip_instead_of_break=p.skip_instead_of_break, block_size=block_size)
+
+
+def random_requests(rng, n, now):
+    reqs = []
+    for i in range(n):
+        state = int(rng.choice([0, 1, 2, 3], p=[0.25, 0.4, 0.15, 0.2]))
+        seg = int(rng.integers(1, 4))
+        ctx = int(rng.integers(0, 6000))
+        r = of.Request(
+            id=int(rng.integers(0, 1 << 40)), arrival=float(rng.uniform(0, now)),
+            last_sched=float(rng.uniform(0, now)) if rng.random() < 0.7 else -1.0,
+            state=state, seg=seg,
+            prev_policy=int(rng.integers(1, 4)) if seg > 1 else 0,
+            cur_policy=int(rng.integers(1, 4)) if state == 3 else 0,
+            seg_ctx=0 if seg == 1 else int(rng.integers(1, 5000)),
+            seg_prefill=int(rng.integers(1, 3000)), pred_out=int(rng.integers(1, 800)),
+            pred_call=float(rng.exponential(0.5)), has_next_call=int(rng.random() < 0.6),
+            ctx_len=ctx, pending=int(rng.integers(0, 2000)) if rng.random() < 0.4 else 0,
+            blocks_on_gpu=0 if state == 2 else -(-ctx // 16), pause_start=float(rng.uniform(0, now)))
+        reqs.append(r)
+    return reqs
+
+
+def _compare(reqs, free_blocks, now, p):
+    want = of.form_batch(reqs, free_blocks, 16, now, p)
+    got = aug.aug_form_batch(_to_c(reqs), free_blocks, now, _c_params(p))
+    assert got["budget"] == want.budget
+    assert got["ids"].tolist() == want.ids
+    assert got["q_len"].tolist() == want.q_len
+    assert got["theta"].view(np.uint64).tolist() == np.array(want.theta, np.float64).view(np.uint64).tolist()
+    assert got["resume_ids"].tolist() == want.resume_ids
+    assert got["park_ids"].tolist() == want.park_ids
+    assert got["free_ids"].tolist() == want.free_ids
+    assert got["policy"].tolist() == want.policy
+    assert got["cost"].view(np.uint64).tolist() == np.array(want.cost, np.float64).view(np.uint64).tolist()
+    return want
+
+
+def test_former_matches_oracle_bit_for_bit_on_random_sets():
+    rng = np.random.default_rng(2024)
+    nonempty = 0
+    for trial in range(300):
+        now = float(rng.uniform(1, 100))
+        p = of.Params(beta=float(rng.choice([0.0, 5e-5, 1e-3])), t_max=int(rng.choice([256, 2048, 8192])),
+                      beta_low=float(rng.choice([0.5, 1.0])), beta_high=float(rng.choice([1.0, 2.0])),
+                      chunk_cap=int(rng.choice([256, 512])), t_iter=float(rng.uniform(0.005, 0.05)),
+                      fwd_a=float(rng.uniform(0.001, 0.05)), fwd_b=float(rng.uniform(1e-9, 1e-6)),
+                      swap_s_per_tok=float(rng.uniform(1e-7, 1e-5)), n_fwd_max=int(rng.integers(1, 8)),
+                      skip_instead_of_break=int(rng.random() < 0.3))
+        reqs = random_requests(rng, int(rng.integers(0, 120)), now)
+        want = _compare(reqs, int(rng.integers(0, 3000)), now, p)
+        nonempty += bool(want.ids)
+        if want.park_ids or want.free_ids:
+            nonempty += 0
+    assert nonempty > 200
+
+
+def test_former_matches_oracle_on_the_2048_token_mixed_batch():
+    from tests.test_oracle_former import _mixed_2048_requests
+    p = of.Params(t_max=2048, beta_low=0.5, beta_high=1.0, chunk_cap=512)
+    want = _compare(_mixed_2048_requests(), 131_072, 2.0, p)
+    assert len(want.ids) == 515
+    _compare(_mixed_2048_requests(extra_decode=True), 131_072, 2.0, p)
+
+
+def test_former_rejects_bad_inputs():
+    p = _c_params(of.Params())
+    bad = _to_c([of.Request(id=1, arrival=0.0, state=1, pred_out=0)])
+    with pytest.raises(AugError):
+        aug.aug_form_batch(bad, 10, 1.0, p)
+    bad = _to_c([of.Request(id=1, arrival=0.0, state=7, pred_out=1)])
+    with pytest.raises(AugError):
+        aug.aug_form_batch(bad, 10, 1.0, p)
+    q = _c_params(of.Params(t_iter=0.0))
+    with pytest.raises(AugError):
+        aug.aug_form_batch(_to_c([]), 10, 1.0, q)
+    assert aug.aug_form_batch(_to_c([]), 10, 1.0, p)["ids"].size == 0
