@@ -112,6 +112,9 @@ def main():
     ap.add_argument("--kv-split", type=int, default=0, help="keys per decode work item (0: planner's choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="before timing, copy a buffer of this many MiB a few times (a kernel of known "
+                         "traffic for calibrating hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; the step needs no "
@@ -171,6 +174,16 @@ def main():
         if timed:
             ev.append((e0, e1))
         return info
+
+    if args.copy_probe_mib > 0:
+        n = args.copy_probe_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy probe: 3 copies of {n} bytes")
+        del src, dst
 
     info = None
     for i in range(args.warmup):

@@ -140,18 +140,6 @@ template <> struct KvFmt<KV_FP8> {
   }
 };
 
-template <int QT>
-__device__ __forceinline__ void load_q(const void* q, int64_t off, float* f) {
-  if constexpr (QT == AUG_F32) {
-    const float4 v = *reinterpret_cast<const float4*>(static_cast<const float*>(q) + off);
-    f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w;
-  } else {
-    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(q) + off);
-    f[0] = bf16_lo(v.x); f[1] = bf16_hi(v.x); f[2] = bf16_lo(v.y); f[3] = bf16_hi(v.y);
-    f[4] = bf16_lo(v.z); f[5] = bf16_hi(v.z); f[6] = bf16_lo(v.w); f[7] = bf16_hi(v.w);
-  }
-}
-
 template <int OT>
 __device__ __forceinline__ void store_out(void* out, int64_t off, float v) {
   if constexpr (OT == AUG_F32) {
@@ -161,6 +149,66 @@ __device__ __forceinline__ void store_out(void* out, int64_t off, float v) {
   }
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b),
+                                         c, false);
+}
+
+// Per-lane query slice and the q.k partial product of one lane's VEC
+// elements. bf16 K against bf16 Q uses packed dot2 on the raw pairs (no
+// conversion of K); other KV formats convert K to fp32 first.
+template <int KVT, int QT> struct RowMath;
+
+template <> struct RowMath<KV_BF16, AUG_BF16> {
+  static constexpr int QW = 4;                 // packed bf16 pairs per lane (8 elements)
+  using q_t = uint32_t;
+  __device__ static void load(const void* q, int64_t off, q_t* dst) {
+    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(q) + off);
+    dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
+  }
+  __device__ static float dot(const q_t* qh, const uint4& k) {
+    float acc = dot2_bf16(k.x, qh[0], 0.f);
+    acc = dot2_bf16(k.y, qh[1], acc);
+    acc = dot2_bf16(k.z, qh[2], acc);
+    return dot2_bf16(k.w, qh[3], acc);
+  }
+};
+
+template <> struct RowMath<KV_F32, AUG_F32> {
+  static constexpr int QW = 4;
+  using q_t = float;
+  __device__ static void load(const void* q, int64_t off, q_t* dst) {
+    const float4 v = *reinterpret_cast<const float4*>(static_cast<const float*>(q) + off);
+    dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
+  }
+  __device__ static float dot(const q_t* qh, const uint4& k) {
+    float acc = qh[0] * __uint_as_float(k.x);
+    acc = fmaf(qh[1], __uint_as_float(k.y), acc);
+    acc = fmaf(qh[2], __uint_as_float(k.z), acc);
+    return fmaf(qh[3], __uint_as_float(k.w), acc);
+  }
+};
+
+template <> struct RowMath<KV_FP8, AUG_BF16> {
+  static constexpr int QW = 8;
+  using q_t = float;
+  __device__ static void load(const void* q, int64_t off, q_t* dst) {
+    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(q) + off);
+    dst[0] = bf16_lo(v.x); dst[1] = bf16_hi(v.x); dst[2] = bf16_lo(v.y); dst[3] = bf16_hi(v.y);
+    dst[4] = bf16_lo(v.z); dst[5] = bf16_hi(v.z); dst[6] = bf16_lo(v.w); dst[7] = bf16_hi(v.w);
+  }
+  __device__ static float dot(const q_t* qh, const uint2& k) {
+    float kf[8];
+    KvFmt<KV_FP8>::to_f32(k, kf);
+    float acc = qh[0] * kf[0];
+#pragma unroll
+    for (int e = 1; e < 8; ++e) acc = fmaf(qh[e], kf[e], acc);
+    return acc;
+  }
+};
+
 // ---------------------------------------------------------------------------
 // row items (VALU)
 // ---------------------------------------------------------------------------
@@ -168,12 +216,13 @@ __device__ __forceinline__ void store_out(void* out, int64_t off, float v) {
 template <int KVT, int D, int G, int QT, int OT>
 __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   using F = KvFmt<KVT>;
+  using M = RowMath<KVT, QT>;
   constexpr int VEC = F::VEC;
   constexpr int LPT = D / VEC;        // lanes per token row
   constexpr int TPI = 64 / LPT;       // tokens per load instruction
   constexpr int NLD = kBlock / TPI;   // load instructions per 16-token block
+  constexpr int EB = KVT == KV_F32 ? 4 : KVT == KV_BF16 ? 2 : 1;
   static_assert(LPT >= 4 && LPT <= 32 && NLD >= 1, "row-path lane mapping");
-  static_assert(QT == AUG_BF16 ? VEC == 8 : VEC == 4, "Q vector width follows KV width");
   using elem_t = typename F::raw_t;
 
   const int lane = threadIdx.x & 63;
@@ -183,16 +232,13 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   const int d0 = dl * VEC;
   const int kvh = it.kind_kvh & 0xFFFF;
 
-  float q[G][VEC];
+  typename M::q_t q[G][M::QW];
   {
     const int64_t qoff = (static_cast<int64_t>(it.q_row0) * a.hq + static_cast<int64_t>(kvh) * G) * D + d0;
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      load_q<QT>(a.q, qoff + static_cast<int64_t>(h) * D, q[h]);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) q[h][e] *= a.scale_log2;
-    }
+    for (int h = 0; h < G; ++h) M::load(a.q, qoff + static_cast<int64_t>(h) * D, q[h]);
   }
+  const float sc = a.scale_log2;
 
   float m[G], l[G], o[G][VEC];
 #pragma unroll
@@ -206,80 +252,96 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   const int blk0 = it.key_begin / kBlock;
   const int nblk = (it.key_end - it.key_begin + kBlock - 1) / kBlock;
   const int64_t head_stride = static_cast<int64_t>(kBlock) * D;   // elements of one (block, head)
+  const char* kc = static_cast<const char*>(a.k_cache);
+  const char* vc = static_cast<const char*>(a.v_cache);
 
-  for (int bi = wave; bi < nblk; bi += kThreads / 64) {
+  // the block id of a wave's next block is fetched one iteration ahead, so
+  // the K/V loads of a block never wait on the block-table load
+  constexpr int kWaves = kThreads / 64;
+  const int32_t* table = a.block_ids + it.bt_off + blk0;
+  int bid_next = wave < nblk ? table[wave] : 0;
+  for (int bi = wave; bi < nblk; bi += kWaves) {
     const int blk = blk0 + bi;
-    const int bid = __builtin_amdgcn_readfirstlane(a.block_ids[it.bt_off + blk]);
+    const int bid = __builtin_amdgcn_readfirstlane(bid_next);
+    if (bi + kWaves < nblk) bid_next = table[bi + kWaves];
     const bool bid_ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
     const int tok0 = blk * kBlock;
-    const int64_t base = (static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride + d0;
+    const int64_t base = ((static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride + d0) * EB;
 
     elem_t kraw[NLD], vraw[NLD];
+    if (bid_ok) {
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      const int t = i * TPI + tsub;
-      if (bid_ok) {
-        kraw[i] = *reinterpret_cast<const elem_t*>(
-            static_cast<const char*>(a.k_cache) + (base + static_cast<int64_t>(t) * D) * (KVT == KV_F32 ? 4 : KVT == KV_BF16 ? 2 : 1));
-        vraw[i] = *reinterpret_cast<const elem_t*>(
-            static_cast<const char*>(a.v_cache) + (base + static_cast<int64_t>(t) * D) * (KVT == KV_F32 ? 4 : KVT == KV_BF16 ? 2 : 1));
-      } else {
+      for (int i = 0; i < NLD; ++i) {
+        const int64_t off = base + static_cast<int64_t>(i * TPI + tsub) * D * EB;
+        kraw[i] = *reinterpret_cast<const elem_t*>(kc + off);
+        vraw[i] = *reinterpret_cast<const elem_t*>(vc + off);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
         kraw[i] = elem_t{};
         vraw[i] = elem_t{};
       }
     }
-    float ksc = 1.f, vsc = 1.f;
+    float ksc = sc, vsc = 1.f;
     if constexpr (KVT == KV_FP8) {
       if (bid_ok) {
-        ksc = a.k_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
+        ksc = sc * a.k_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
         vsc = a.v_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
       }
     }
+    // a block is either entirely inside the span (no masking at all) or the
+    // span's tail block / an unusable block (masked token by token)
+    const bool full = bid_ok && tok0 + kBlock <= it.key_end;
 
     float s[NLD][G];
-    bool valid[NLD];
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      valid[i] = bid_ok && (tok0 + i * TPI + tsub) < it.key_end;
-      float kf[VEC];
-      F::to_f32(kraw[i], kf);
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        float acc = 0.f;
+      for (int h = 0; h < G; ++h) s[i][h] = group_sum<LPT>(M::dot(q[h], kraw[i])) * ksc;
+    }
+    if (!full) {
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc += q[h][e] * kf[e];
-        acc = group_sum<LPT>(acc) * ksc;
-        s[i][h] = valid[i] ? acc : -INFINITY;
+      for (int i = 0; i < NLD; ++i) {
+        const bool valid = bid_ok && (tok0 + i * TPI + tsub) < it.key_end;
+#pragma unroll
+        for (int h = 0; h < G; ++h) s[i][h] = valid ? s[i][h] : -INFINITY;
+        if (!valid) vraw[i] = elem_t{};   // zero, so 0 * value never meets NaN
       }
     }
 
+    float mn[G];
+    bool moved = false;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       float mb = s[0][h];
 #pragma unroll
       for (int i = 1; i < NLD; ++i) mb = fmaxf(mb, s[i][h]);
-      const float mn = fmaxf(m[h], mb);
-      const float alpha = __builtin_amdgcn_exp2f(m[h] - mn);
-      m[h] = mn;
-      float psum = 0.f;
-      float p[NLD];
+      mn[h] = fmaxf(m[h], mb);
+      moved |= mn[h] != m[h];
+    }
+    // rescale only when some running maximum moved (alpha is exactly 1 otherwise)
+    if (__any(moved)) {
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) {
-        p[i] = __builtin_amdgcn_exp2f(s[i][h] - mn);
-        psum += p[i];
+      for (int h = 0; h < G; ++h) {
+        const float alpha = __builtin_amdgcn_exp2f(m[h] - mn[h]);
+        l[h] *= alpha;
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[h][e] *= alpha;
+        m[h] = mn[h];
       }
-      l[h] = l[h] * alpha + psum;
+    }
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) o[h][e] *= alpha;
+    for (int i = 0; i < NLD; ++i) {
+      float vf[VEC];
+      F::to_f32(vraw[i], vf);
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) p[i] *= vsc;
-      // accumulate p_i * v_i (values of masked tokens are never touched)
+      for (int h = 0; h < G; ++h) {
+        const float p = __builtin_amdgcn_exp2f(s[i][h] - m[h]);
+        l[h] += p;
+        const float pv = p * vsc;
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) {
-        float vf[VEC];
-        F::to_f32(vraw[i], vf);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) o[h][e] += valid[i] ? p[i] * vf[e] : 0.f;
+        for (int e = 0; e < VEC; ++e) o[h][e] = fmaf(pv, vf[e], o[h][e]);
       }
     }
   }
@@ -563,25 +625,77 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
   row_item<KVT, D, G, QT, OT>(it, a, reinterpret_cast<float*>(smem));
 }
 
+// Merge the split-K partials of each (row, KV head): O = sum_s o_s 2^(m_s-M) /
+// sum_s l_s 2^(m_s-M), M = max_s m_s. The (m, l) pairs of all partials are
+// staged in LDS first so the output loads of every partial are independent.
+constexpr int kMaxMergeStage = 64;   // partials staged per pass
+
 template <int D, int G, int OT>
 __global__ __launch_bounds__(kThreads) void merge_kernel(const MergeGroup* groups, const float* partials,
                                                          void* out, int32_t hq) {
+  __shared__ float ml[kMaxMergeStage][2 * G];
   const MergeGroup g = groups[blockIdx.x];
   const int64_t pf = aug::partial_floats(G, D);
-  for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
+  constexpr int PER = (G * D + kThreads - 1) / kThreads;   // output elements per thread
+  float acc[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) acc[k] = 0.f;
+  float run_m[G], run_l[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    run_m[h] = kNegBig;
+    run_l[h] = 0.f;
+  }
+  for (int s0 = 0; s0 < g.n_parts; s0 += kMaxMergeStage) {
+    const int ns = min(kMaxMergeStage, g.n_parts - s0);
+    __syncthreads();
+    for (int i = threadIdx.x; i < ns * 2 * G; i += kThreads) {
+      const int s = i / (2 * G);
+      const int j = i % (2 * G);
+      ml[s][j] = partials[(g.part0 + s0 + s) * pf + G * D + j];
+    }
+    __syncthreads();
+    // per head: the pass maximum, rescaling of what earlier passes summed
+    float pm[G], scale_old[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float m = run_m[h];
+      for (int s = 0; s < ns; ++s) m = fmaxf(m, ml[s][h]);
+      scale_old[h] = __builtin_amdgcn_exp2f(run_m[h] - m);
+      pm[h] = m;
+      float l = run_l[h] * scale_old[h];
+      for (int s = 0; s < ns; ++s) l += ml[s][G + h] * __builtin_amdgcn_exp2f(ml[s][h] - m);
+      run_l[h] = l;
+      run_m[h] = m;
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = threadIdx.x + k * kThreads;
+      if (idx >= G * D) break;
+      const int h = idx / D;
+      float o = acc[k] * scale_old[h];
+      const float* base = partials + static_cast<int64_t>(g.part0 + s0) * pf + idx;
+      int s = 0;
+      for (; s + 4 <= ns; s += 4) {
+        const float o0 = base[(s + 0) * pf], o1 = base[(s + 1) * pf];
+        const float o2 = base[(s + 2) * pf], o3 = base[(s + 3) * pf];
+        o += o0 * __builtin_amdgcn_exp2f(ml[s + 0][h] - pm[h]);
+        o += o1 * __builtin_amdgcn_exp2f(ml[s + 1][h] - pm[h]);
+        o += o2 * __builtin_amdgcn_exp2f(ml[s + 2][h] - pm[h]);
+        o += o3 * __builtin_amdgcn_exp2f(ml[s + 3][h] - pm[h]);
+      }
+      for (; s < ns; ++s) o += base[s * pf] * __builtin_amdgcn_exp2f(ml[s][h] - pm[h]);
+      acc[k] = o;
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = threadIdx.x + k * kThreads;
+    if (idx >= G * D) break;
     const int h = idx / D;
     const int d = idx % D;
-    float mx = kNegBig;
-    for (int s = 0; s < g.n_parts; ++s) mx = fmaxf(mx, partials[(g.part0 + s) * pf + G * D + h]);
-    float ls = 0.f, os = 0.f;
-    for (int s = 0; s < g.n_parts; ++s) {
-      const float* pp = partials + (g.part0 + s) * pf;
-      const float f = __builtin_amdgcn_exp2f(pp[G * D + h] - mx);
-      ls += pp[G * D + G + h] * f;
-      os += pp[h * D + d] * f;
-    }
     const int64_t off = (static_cast<int64_t>(g.q_row) * hq + static_cast<int64_t>(g.kvh) * G + h) * D + d;
-    store_out<OT>(out, off, os / ls);
+    store_out<OT>(out, off, acc[k] / run_l[h]);
   }
 }
 

@@ -66,12 +66,13 @@ struct Sized {
 
 int32_t choose_split(int64_t total_row_keys, int32_t requested) {
   if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;
-  // Aim at ~12 row items per compute unit (256 CUs), but keep each at least
-  // 256 keys long so its fixed costs stay small.
-  const int64_t target_items = 256 * 12;
-  int64_t s = (total_row_keys + target_items - 1) / std::max<int64_t>(target_items, 1);
+  // About four row items per compute unit (256 CUs) on small batches; on
+  // large ones spans of 4096 keys, long enough that an item's fixed costs
+  // (query load, state merge, partial write) are a few percent of its
+  // streaming time while lognormal context mixes still balance.
+  int64_t s = (total_row_keys + 1023) / 1024;
   s = std::max<int64_t>(s, 256);
-  s = std::min<int64_t>(s, 1 << 20);
+  s = std::min<int64_t>(s, 4096);
   return static_cast<int32_t>(((s + kBlock - 1) / kBlock) * kBlock);
 }
 
