@@ -213,7 +213,7 @@ template <> struct RowMath<KV_FP8, AUG_BF16> {
 // row items (VALU)
 // ---------------------------------------------------------------------------
 
-template <int KVT, int D, int G, int QT, int OT>
+template <int KVT, int D, int G, int QT, int OT, bool PREFETCH>
 __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   using F = KvFmt<KVT>;
   using M = RowMath<KVT, QT>;
@@ -255,34 +255,60 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   const char* kc = static_cast<const char*>(a.k_cache);
   const char* vc = static_cast<const char*>(a.v_cache);
 
-  // the block id of a wave's next block is fetched one iteration ahead, so
-  // the K/V loads of a block never wait on the block-table load
+  // The block id of a wave's next block is fetched one iteration ahead, so
+  // the K/V loads of a block never wait on the block-table load. With
+  // PREFETCH the K/V of the next block are in flight too while the current
+  // one is computed (used where occupancy is low anyway).
   constexpr int kWaves = kThreads / 64;
   const int32_t* table = a.block_ids + it.bt_off + blk0;
-  int bid_next = wave < nblk ? table[wave] : 0;
-  for (int bi = wave; bi < nblk; bi += kWaves) {
-    const int blk = blk0 + bi;
-    const int bid = __builtin_amdgcn_readfirstlane(bid_next);
-    if (bi + kWaves < nblk) bid_next = table[bi + kWaves];
-    const bool bid_ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
-    const int tok0 = blk * kBlock;
+  auto load_block = [&](int bid, elem_t* kr, elem_t* vr) {
+    const bool ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
     const int64_t base = ((static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride + d0) * EB;
-
-    elem_t kraw[NLD], vraw[NLD];
-    if (bid_ok) {
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) {
+    for (int i = 0; i < NLD; ++i) {
+      if (ok) {
         const int64_t off = base + static_cast<int64_t>(i * TPI + tsub) * D * EB;
-        kraw[i] = *reinterpret_cast<const elem_t*>(kc + off);
-        vraw[i] = *reinterpret_cast<const elem_t*>(vc + off);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < NLD; ++i) {
-        kraw[i] = elem_t{};
-        vraw[i] = elem_t{};
+        kr[i] = *reinterpret_cast<const elem_t*>(kc + off);
+        vr[i] = *reinterpret_cast<const elem_t*>(vc + off);
+      } else {
+        kr[i] = elem_t{};
+        vr[i] = elem_t{};
       }
     }
+  };
+  int bid_next = wave < nblk ? table[wave] : 0;
+  elem_t kpre[PREFETCH ? NLD : 1], vpre[PREFETCH ? NLD : 1];
+  int bid_pre = 0;
+  if constexpr (PREFETCH) {
+    if (wave < nblk) {
+      bid_pre = __builtin_amdgcn_readfirstlane(bid_next);
+      load_block(bid_pre, kpre, vpre);
+      if (wave + kWaves < nblk) bid_next = table[wave + kWaves];
+    }
+  }
+  for (int bi = wave; bi < nblk; bi += kWaves) {
+    const int blk = blk0 + bi;
+    int bid;
+    elem_t kraw[NLD], vraw[NLD];
+    if constexpr (PREFETCH) {
+      bid = bid_pre;
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        kraw[i] = kpre[i];
+        vraw[i] = vpre[i];
+      }
+      if (bi + kWaves < nblk) {
+        bid_pre = __builtin_amdgcn_readfirstlane(bid_next);
+        load_block(bid_pre, kpre, vpre);
+        if (bi + 2 * kWaves < nblk) bid_next = table[bi + 2 * kWaves];
+      }
+    } else {
+      bid = __builtin_amdgcn_readfirstlane(bid_next);
+      if (bi + kWaves < nblk) bid_next = table[bi + kWaves];
+      load_block(bid, kraw, vraw);
+    }
+    const bool bid_ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
+    const int tok0 = blk * kBlock;
     float ksc = sc, vsc = 1.f;
     if constexpr (KVT == KV_FP8) {
       if (bid_ok) {
@@ -470,9 +496,9 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
   const int64_t head_stride = static_cast<int64_t>(kBlock) * D;
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int k0 = t * 64;
-    uint4 kr[KPT], vr[KPT];
+  // K/V of key tile t+1 are loaded into registers while tile t is computed
+  uint4 kr[KPT], vr[KPT];
+  auto load_tile = [&](int k0) {
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
       const int tok = k0 + tk * KPT + u;
@@ -488,6 +514,10 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
         }
       }
     }
+  };
+  load_tile(0);
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = t * 64;
     __syncthreads();   // the previous tile's LDS reads are done
 #pragma unroll
     for (int u = 0; u < KPT; ++u)
@@ -509,6 +539,7 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       }
     }
     __syncthreads();
+    if (t + 1 < ntiles) load_tile(k0 + 64);
 
     // S^T = K Q^T for keys k0..k0+63
     f32x16_t sacc[2];
@@ -611,7 +642,7 @@ template <int D, int G>
 constexpr int row_lds_bytes() { return (kThreads / 64) * G * (D + 2) * 4; }
 
 template <int KVT, int D, int G, int QT, int OT, bool TILES>
-__global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
+__device__ __forceinline__ void attn_body(const AttnArgs& a) {
   constexpr int RB = row_lds_bytes<D, G>();
   constexpr int TB = TILES ? TileLds<D>::BYTES : 0;
   __shared__ __align__(16) unsigned char smem[RB > TB ? RB : TB];
@@ -622,7 +653,21 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a) {
       return;
     }
   }
-  row_item<KVT, D, G, QT, OT>(it, a, reinterpret_cast<float*>(smem));
+  row_item<KVT, D, G, QT, OT, TILES>(it, a, reinterpret_cast<float*>(smem));
+}
+
+// Batches without prefill tiles: row items only, sized for high occupancy.
+template <int KVT, int D, int G, int QT, int OT>
+__global__ __launch_bounds__(kThreads) void attn_rows_kernel(AttnArgs a) {
+  attn_body<KVT, D, G, QT, OT, false>(a);
+}
+
+// Mixed batches: MFMA tiles and row items in one launch. The tile path's
+// accumulators set the register budget (two waves per SIMD); the row path
+// spends the same budget on prefetching the next block.
+template <int KVT, int D, int G, int QT, int OT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mixed_kernel(AttnArgs a) {
+  attn_body<KVT, D, G, QT, OT, true>(a);
 }
 
 // Merge the split-K partials of each (row, KV head): O = sum_s o_s 2^(m_s-M) /
@@ -705,12 +750,12 @@ aug_status launch(const AttnArgs& a, const aug_attn_plan_info& info, const Merge
   if (info.num_items > 0) {
     if (info.num_prefill_items > 0) {
       if constexpr (KVT == KV_BF16 && QT == AUG_BF16) {
-        hipLaunchKernelGGL((attn_kernel<KVT, D, G, QT, OT, true>), dim3(info.num_items), dim3(kThreads), 0, st, a);
+        hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT>), dim3(info.num_items), dim3(kThreads), 0, st, a);
       } else {
         return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: plan has tiles for a dtype set without them");
       }
     } else {
-      hipLaunchKernelGGL((attn_kernel<KVT, D, G, QT, OT, false>), dim3(info.num_items), dim3(kThreads), 0, st, a);
+      hipLaunchKernelGGL((attn_rows_kernel<KVT, D, G, QT, OT>), dim3(info.num_items), dim3(kThreads), 0, st, a);
     }
     if (hipError_t e = hipGetLastError(); e != hipSuccess)
       return aug::fail(AUG_ERR_HIP, "aug_attn_mixed: launch failed: %s", hipGetErrorString(e));
