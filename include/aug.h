@@ -71,7 +71,8 @@ typedef enum { AUG_POL_NONE = 0, AUG_PRESERVE = 1, AUG_DISCARD = 2, AUG_SWAP = 3
  *   head_dim: 64 or 128.  block_size: 16 (tokens per KV block).
  *   Supported dtype sets (q, kv, out): (F32, F32, F32), (BF16, BF16, BF16),
  *   (BF16, FP8_E4M3FN, BF16).
- *   softmax_scale: multiplies q.k before the softmax (typically 1/sqrt(head_dim)). */
+ *   softmax_scale: multiplies q.k before the softmax (typically 1/sqrt(head_dim));
+ *   finite and > 0. */
 typedef struct {
   int32_t num_q_heads;
   int32_t num_kv_heads;

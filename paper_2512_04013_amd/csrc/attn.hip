@@ -88,6 +88,14 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
   return u >> 16;
 }
 
+typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
+
+// two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  const bf16x2v_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
@@ -230,7 +238,7 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   const int dl = lane % LPT;
   const int tsub = lane / LPT;
   const int d0 = dl * VEC;
-  const int kvh = it.kind_kvh & 0xFFFF;
+  const int kvh = it.kvh;
 
   typename M::q_t q[G][M::QW];
   {
@@ -444,11 +452,17 @@ template <int D>
 struct TileLds {
   static constexpr int KS = D + 8;    // K row stride (elements): 16-byte aligned, conflict-free reads
   static constexpr int VS = 64 + 4;   // V^T row stride (elements)
-  static constexpr int BYTES = (64 * KS + D * VS) * 2;
+  static constexpr int STAGE = (64 * KS + D * VS) * 2;   // bytes of one K + V^T stage
+  static constexpr int IDS = aug::kTileSplit / kBlock + 8; // block ids of one item's key span
+  static constexpr int BYTES = 2 * STAGE + IDS * 4;      // double-buffered stages + ids
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
+// One tile item: up to 128 query rows (kTileRows / G positions x G heads of
+// one KV head) against keys [key_begin, key_end) of the request. Key tiles of
+// 64 go through two LDS stages: while tile t is multiplied, tile t+1 sits in
+// the other stage and tile t+2 is on its way from HBM into registers.
 template <int D, int G, int OT>
 __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* smem) {
   using L = TileLds<D>;
@@ -457,14 +471,12 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   constexpr int CPR = D / 8;          // 16-byte chunks per key row
   constexpr int KPT = 64 * CPR / kThreads;   // keys staged per thread (4 or 2)
   static_assert(KPT == 2 || KPT == 4, "tile staging map");
-  uint16_t* ks = reinterpret_cast<uint16_t*>(smem);
-  uint16_t* vt = ks + 64 * L::KS;
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int n = lane & 31;            // MFMA column: query row within the wave
   const int hh = lane >> 5;           // lane half: which 8 of the 16 k-slots
-  const int kvh = it.kind_kvh & 0xFFFF;
+  const int kvh = it.kvh;
   const int row = wave * 32 + n;
   const int p = row / G;
   const int gh = row % G;
@@ -491,12 +503,20 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   const int tc = threadIdx.x % CPR;
   const int tk = threadIdx.x / CPR;
   const int key_end = it.key_end;
-  const int ntiles = (key_end + 63) / 64;
+  const int t0 = it.key_begin / 64;
+  const int t1 = (key_end + 63) / 64;
   const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
   const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
   const int64_t head_stride = static_cast<int64_t>(kBlock) * D;
 
-  // K/V of key tile t+1 are loaded into registers while tile t is computed
+  // the item's block ids (at most IDS: spans are capped by the planner) are
+  // read once into LDS, so staging a key tile costs one round trip
+  int32_t* ids = reinterpret_cast<int32_t*>(smem + 2 * L::STAGE);
+  const int blk_first = it.key_begin / kBlock;
+  const int n_ids = (key_end + kBlock - 1) / kBlock - blk_first;
+  for (int i = threadIdx.x; i < n_ids && i < L::IDS; i += kThreads) ids[i] = a.block_ids[it.bt_off + blk_first + i];
+  __syncthreads();
+
   uint4 kr[KPT], vr[KPT];
   auto load_tile = [&](int k0) {
 #pragma unroll
@@ -505,7 +525,7 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       kr[u] = uint4{0, 0, 0, 0};
       vr[u] = uint4{0, 0, 0, 0};
       if (tok < key_end) {
-        const int bid = a.block_ids[it.bt_off + (tok >> 4)];
+        const int bid = ids[(tok >> 4) - blk_first];
         if (static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks)) {
           const int64_t off = (static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride +
                               static_cast<int64_t>(tok & 15) * D + 8 * tc;
@@ -515,10 +535,9 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       }
     }
   };
-  load_tile(0);
-  for (int t = 0; t < ntiles; ++t) {
-    const int k0 = t * 64;
-    __syncthreads();   // the previous tile's LDS reads are done
+  auto store_tile = [&](int stage) {
+    uint16_t* ks = reinterpret_cast<uint16_t*>(smem + stage * L::STAGE);
+    uint16_t* vt = ks + 64 * L::KS;
 #pragma unroll
     for (int u = 0; u < KPT; ++u)
       *reinterpret_cast<uint4*>(ks + (tk * KPT + u) * L::KS + 8 * tc) = kr[u];
@@ -538,8 +557,21 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
         *reinterpret_cast<uint32_t*>(dst) = w[0] | (w[1] << 16);
       }
     }
-    __syncthreads();
-    if (t + 1 < ntiles) load_tile(k0 + 64);
+  };
+
+  load_tile(t0 * 64);
+  store_tile(0);
+  if (t0 + 1 < t1) load_tile((t0 + 1) * 64);
+  for (int t = t0; t < t1; ++t) {
+    const int k0 = t * 64;
+    const int stage = (t - t0) & 1;
+    __syncthreads();   // stage `stage` is written; the other stage's readers are done
+    if (t + 1 < t1) {
+      store_tile(stage ^ 1);
+      if (t + 2 < t1) load_tile(k0 + 128);
+    }
+    const uint16_t* ks = reinterpret_cast<const uint16_t*>(smem + stage * L::STAGE);
+    const uint16_t* vt = ks + 64 * L::KS;
 
     // S^T = K Q^T for keys k0..k0+63
     f32x16_t sacc[2];
@@ -554,39 +586,47 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       }
     }
 
-    // online softmax over this row's 64 keys (32 in each lane half)
-    const bool need_mask = k0 + 63 > it.pos0;
-    float smax = kNegBig;
+    // online softmax over this row's 64 keys (32 in each lane half), in the
+    // log2 domain: p = 2^(s*c - m). Keys past the row's position (or past
+    // key_end) are masked. The running output is rescaled only when some
+    // row's maximum moved (the factor is exactly 1 otherwise).
+    const bool need_mask = k0 + 63 > it.pos0 || k0 + 64 > key_end;
+    if (need_mask) {
+      // entry (mb, i, j) of this lane is key k0 + 32mb + 8i + 4hh + j
+      const int lim = min(pos, key_end - 1) - k0 - 4 * hh;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (32 * mb + 8 * i + j > lim) sacc[mb][4 * i + j] = -INFINITY;
+    }
+    float smax = sacc[0][0];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int key = k0 + 32 * mb + 8 * i + 4 * hh + j;
-          float v = sacc[mb][4 * i + j] * c;
-          if (need_mask && key > pos) v = -INFINITY;
-          sacc[mb][4 * i + j] = v;
-          smax = fmaxf(smax, v);
-        }
+      for (int e = (mb == 0 ? 1 : 0); e < 16; ++e) smax = fmaxf(smax, sacc[mb][e]);
     smax = fmaxf(smax, __shfl_xor(smax, 32));
-    const float mn = fmaxf(m_run, smax);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
-    m_run = mn;
-    float psum = 0.f;
+    const float mn = fmaxf(m_run, smax * c);
+    if (__any(mn != m_run)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc_o[db][e] *= alpha;
+      m_run = mn;
+    }
+    const float neg_m = -m_run;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float pv = __builtin_amdgcn_exp2f(sacc[mb][e] - mn);
+        const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[mb][e], c, neg_m));
         sacc[mb][e] = pv;
-        psum += pv;
+        l_run += pv;
       }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc_o[db][e] *= alpha;
 
     // O^T += V^T P^T, 16 keys per step; k-slots of lane half hh are keys
     // {16s+4hh+j, 16s+8+4hh+j}, exactly the S^T entries this lane holds
@@ -595,10 +635,10 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       const int mb = s >> 1;
       const int i0 = 2 * (s & 1);
       uint4 pw;
-      pw.x = f32_to_bf16_bits(sacc[mb][4 * i0 + 0]) | (f32_to_bf16_bits(sacc[mb][4 * i0 + 1]) << 16);
-      pw.y = f32_to_bf16_bits(sacc[mb][4 * i0 + 2]) | (f32_to_bf16_bits(sacc[mb][4 * i0 + 3]) << 16);
-      pw.z = f32_to_bf16_bits(sacc[mb][4 * i0 + 4]) | (f32_to_bf16_bits(sacc[mb][4 * i0 + 5]) << 16);
-      pw.w = f32_to_bf16_bits(sacc[mb][4 * i0 + 6]) | (f32_to_bf16_bits(sacc[mb][4 * i0 + 7]) << 16);
+      pw.x = pack_bf16(sacc[mb][4 * i0 + 0], sacc[mb][4 * i0 + 1]);
+      pw.y = pack_bf16(sacc[mb][4 * i0 + 2], sacc[mb][4 * i0 + 3]);
+      pw.z = pack_bf16(sacc[mb][4 * i0 + 4], sacc[mb][4 * i0 + 5]);
+      pw.w = pack_bf16(sacc[mb][4 * i0 + 6], sacc[mb][4 * i0 + 7]);
       const bf16x8_t pop = as_bf16x8(pw);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -612,7 +652,8 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (row_ok) {
+  if (!row_ok) return;
+  if (it.part < 0) {
     const float inv = 1.f / l_tot;
     const int64_t ooff = (static_cast<int64_t>(it.q_row0 + p) * a.hq + static_cast<int64_t>(kvh) * G + gh) * D;
 #pragma unroll
@@ -622,8 +663,8 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
         const int dim = 32 * db + 8 * i + 4 * hh;
         if constexpr (OT == AUG_BF16) {
           uint2 w;
-          w.x = f32_to_bf16_bits(acc_o[db][4 * i + 0] * inv) | (f32_to_bf16_bits(acc_o[db][4 * i + 1] * inv) << 16);
-          w.y = f32_to_bf16_bits(acc_o[db][4 * i + 2] * inv) | (f32_to_bf16_bits(acc_o[db][4 * i + 3] * inv) << 16);
+          w.x = pack_bf16(acc_o[db][4 * i + 0] * inv, acc_o[db][4 * i + 1] * inv);
+          w.y = pack_bf16(acc_o[db][4 * i + 2] * inv, acc_o[db][4 * i + 3] * inv);
           *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + ooff + dim) = w;
         } else {
           float4 w{acc_o[db][4 * i] * inv, acc_o[db][4 * i + 1] * inv, acc_o[db][4 * i + 2] * inv,
@@ -631,6 +672,21 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
           *reinterpret_cast<float4*>(static_cast<float*>(a.out) + ooff + dim) = w;
         }
       }
+  } else {
+    // split tile: unnormalised partial of this row for head gh
+    float* pp = a.partials + static_cast<int64_t>(it.part + p * it.part_stride) * aug::partial_floats(G, D);
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int dim = 32 * db + 8 * i + 4 * hh;
+        *reinterpret_cast<float4*>(pp + gh * D + dim) =
+            float4{acc_o[db][4 * i], acc_o[db][4 * i + 1], acc_o[db][4 * i + 2], acc_o[db][4 * i + 3]};
+      }
+    if (hh == 0) {
+      pp[G * D + gh] = m_run;
+      pp[G * D + G + gh] = l_tot;
+    }
   }
 }
 
@@ -648,7 +704,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   __shared__ __align__(16) unsigned char smem[RB > TB ? RB : TB];
   const WorkItem it = a.items[blockIdx.x];
   if constexpr (TILES) {
-    if ((it.kind_kvh >> 16) == aug::kTileItem) {
+    if (it.kind == aug::kTileItem) {
       tile_item<D, G, OT>(it, a, smem);
       return;
     }

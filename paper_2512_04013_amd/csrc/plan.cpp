@@ -51,8 +51,8 @@ aug_status check_shape(const aug_attn_shape* s, const char* who) {
                 s->kv_dtype, s->out_dtype);
   if (s->kv_dtype == AUG_FP8_E4M3FN && s->head_dim != 128)
     return fail(AUG_ERR_UNSUPPORTED, "%s: fp8 KV needs head_dim 128", who);
-  if (!std::isfinite(s->softmax_scale))
-    return fail(AUG_ERR_INVALID, "%s: softmax_scale is not finite", who);
+  if (!std::isfinite(s->softmax_scale) || !(s->softmax_scale > 0.f))
+    return fail(AUG_ERR_INVALID, "%s: softmax_scale must be finite and positive", who);
   return AUG_OK;
 }
 
@@ -60,9 +60,20 @@ namespace {
 
 struct Sized {
   WorkItem item;
-  int64_t weight;   // sort key: longest first
+  double weight;    // estimated ns: longest first
   int64_t order;    // creation order, to keep the sort deterministic
 };
+
+// Estimated run time of a work item while the GPU is full (about 512
+// workgroups resident), used only to order items longest first so that
+// prefill tiles (compute bound) run beside decode spans (memory bound) and no
+// long item starts last. Calibrated on MI355X: a row item streams its K/V at
+// about 11.5 GB/s per resident workgroup (5.9 TB/s over 512), a 64-key MFMA
+// tile step of 128 rows takes about 5 us.
+double row_item_ns(int64_t keys, int32_t head_dim, int32_t kv_bytes) {
+  return static_cast<double>(keys) * head_dim * kv_bytes * 2 / 11.5;
+}
+double tile_item_ns(int64_t key_tiles) { return static_cast<double>(key_tiles) * 5000.0; }
 
 int32_t choose_split(int64_t total_row_keys, int32_t requested) {
   if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;
@@ -133,10 +144,13 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   // requests by span length orders their items longest first.
   struct RowReq {
     int32_t r, span, nspan;
+    double ns;      // estimated time of one of its items
   };
+  const int32_t kv_bytes = s->kv_dtype == AUG_F32 ? 4 : s->kv_dtype == AUG_BF16 ? 2 : 1;
   std::vector<RowReq> row_reqs;
   std::vector<Sized> tiles;
-  int64_t n_row_items = 0, n_groups = 0, n_parts = 0;
+  std::vector<MergeGroup> tile_groups;
+  int64_t n_row_items = 0, n_groups = 0, tile_parts = 0, row_parts = 0;
   int64_t order = 0;
   for (int32_t r = 0; r < n; ++r) {
     const int32_t q = b->q_start[r + 1] - b->q_start[r];
@@ -145,17 +159,38 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
       for (int32_t j0 = 0; j0 < q; j0 += pos_per_tile) {
         const int32_t nr = std::min(pos_per_tile, q - j0);
         const int32_t pos0 = ctx - q + j0;
+        const int32_t key_end = pos0 + nr;
+        // long tiles are split into near-equal spans of whole key tiles; each
+        // row of a split tile then has one partial per span, stored together
+        const int32_t nsplit = (key_end + kTileSplit - 1) / kTileSplit;
+        int32_t span = (key_end + nsplit - 1) / nsplit;
+        span = ((span + kKeyTile - 1) / kKeyTile) * kKeyTile;
+        const int32_t nsp = (key_end + span - 1) / span;
+        static_assert(kTileSplit % kKeyTile == 0, "tile spans are whole key tiles");
+        // span <= kTileSplit, so the kernel's per-item block-id buffer suffices
         for (int32_t h = 0; h < hkv; ++h) {
-          WorkItem it{};
-          it.kind_kvh = h | (kTileItem << 16);
-          it.q_row0 = b->q_start[r] + j0;
-          it.n_rows = nr;
-          it.key_begin = 0;
-          it.key_end = pos0 + nr;
-          it.pos0 = pos0;
-          it.bt_off = b->bt_start[r];
-          it.part = -1;
-          tiles.push_back({it, static_cast<int64_t>(nr) * it.key_end, order++});   // work ~ rows x keys
+          for (int32_t sidx = 0; sidx < nsp; ++sidx) {
+            WorkItem it{};
+            it.kvh = static_cast<int16_t>(h);
+            it.kind = kTileItem;
+            it.q_row0 = b->q_start[r] + j0;
+            it.n_rows = static_cast<int16_t>(nr);
+            it.part_stride = static_cast<int16_t>(nsp);
+            it.key_begin = sidx * span;
+            it.key_end = std::min(key_end, (sidx + 1) * span);
+            it.pos0 = pos0;
+            it.bt_off = b->bt_start[r];
+            it.part = nsp > 1 ? static_cast<int32_t>(tile_parts) + sidx : -1;
+            const int64_t steps = (it.key_end - it.key_begin + kKeyTile - 1) / kKeyTile;
+            tiles.push_back({it, tile_item_ns(steps), order++});
+          }
+          if (nsp > 1) {
+            for (int32_t j = 0; j < nr; ++j)
+              tile_groups.push_back(MergeGroup{b->q_start[r] + j0 + j, h,
+                                               static_cast<int32_t>(tile_parts) + j * nsp, nsp});
+            tile_parts += static_cast<int64_t>(nr) * nsp;
+            n_groups += nr;
+          }
         }
       }
       continue;
@@ -165,14 +200,14 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
     const int32_t nspan = (keys + split - 1) / split;
     int32_t span = (keys + nspan - 1) / nspan;
     span = ((span + kBlock - 1) / kBlock) * kBlock;
-    row_reqs.push_back({r, span, (keys + span - 1) / span});
+    row_reqs.push_back({r, span, (keys + span - 1) / span, row_item_ns(span, s->head_dim, kv_bytes)});
     for (int32_t j = 0; j < q; ++j) {
       const int32_t k = ctx - q + j + 1;
       const int64_t ns = (k + span - 1) / span;
       n_row_items += ns * hkv;
       if (ns > 1) {
         n_groups += hkv;
-        n_parts += ns * hkv;
+        row_parts += ns * hkv;
       }
     }
   }
@@ -181,7 +216,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
     return a.order < c.order;
   });
   std::stable_sort(row_reqs.begin(), row_reqs.end(),
-                   [](const RowReq& a, const RowReq& c) { return a.span > c.span; });
+                   [](const RowReq& a, const RowReq& c) { return a.ns > c.ns; });
   (void)order;
 
   const int64_t n_items = static_cast<int64_t>(tiles.size()) + n_row_items;
@@ -189,6 +224,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
     return fail(AUG_ERR_UNSUPPORTED, "%s: %lld work items", who, (long long)n_items);
   const int64_t items_off = sizeof(PlanHeader);
   const int64_t groups_off = items_off + n_items * static_cast<int64_t>(sizeof(WorkItem));
+  const int64_t n_parts = tile_parts + row_parts;
   if (n_parts > (int64_t{1} << 30))
     return fail(AUG_ERR_UNSUPPORTED, "%s: %lld split-K partials", who, (long long)n_parts);
   const int64_t plan_bytes = groups_off + n_groups * static_cast<int64_t>(sizeof(MergeGroup));
@@ -225,9 +261,15 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   auto* items = reinterpret_cast<WorkItem*>(base + items_off);
   auto* groups = reinterpret_cast<MergeGroup*>(base + groups_off);
   size_t k = 0;
-  for (const Sized& t : tiles) items[k++] = t.item;
-  int32_t parts = 0, ng = 0;
+  int32_t ng = 0;
+  for (const MergeGroup& mg : tile_groups) groups[ng++] = mg;
+  int32_t parts = static_cast<int32_t>(tile_parts);
+  size_t ti = 0;
+  auto emit_tiles_longer_than = [&](double ns) {
+    while (ti < tiles.size() && tiles[ti].weight >= ns) items[k++] = tiles[ti++].item;
+  };
   for (const RowReq& rr : row_reqs) {
+    emit_tiles_longer_than(rr.ns);
     const int32_t r = rr.r;
     const int32_t q = b->q_start[r + 1] - b->q_start[r];
     const int32_t ctx = b->ctx_len[r];
@@ -243,9 +285,11 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
         }
         for (int32_t sidx = 0; sidx < nspan; ++sidx) {
           WorkItem it{};
-          it.kind_kvh = h | (kRowItem << 16);
+          it.kvh = static_cast<int16_t>(h);
+          it.kind = kRowItem;
           it.q_row0 = b->q_start[r] + j;
           it.n_rows = 1;
+          it.part_stride = 1;
           it.key_begin = sidx * rr.span;
           it.key_end = std::min(keys, (sidx + 1) * rr.span);
           it.pos0 = pos;
@@ -256,5 +300,6 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
       }
     }
   }
+  emit_tiles_longer_than(-1.0);
   return AUG_OK;
 }

@@ -11,6 +11,7 @@ constexpr int32_t kPlanVersion = 1;
 constexpr int32_t kBlock = 16;              // tokens per KV block
 constexpr int32_t kKeyTile = 64;            // keys per MFMA tile (4 blocks)
 constexpr int32_t kTileRows = 128;          // query rows (positions x group heads) per MFMA tile
+constexpr int32_t kTileSplit = 1024;        // keys per split of a long tile
 
 enum ItemKind : int32_t {
   kRowItem = 0,   // one query row (all heads of one KV head group) against a key span, VALU
@@ -32,14 +33,17 @@ struct PlanHeader {          // 64 bytes
 };
 
 struct WorkItem {            // 32 bytes
-  int32_t kind_kvh;          // KV head | kind << 16
+  int16_t kvh;               // KV head
+  int8_t kind;               // ItemKind
+  int8_t reserved;
   int32_t q_row0;            // first global row of Q/O
-  int32_t n_rows;            // rows (context positions) in the item
-  int32_t key_begin;         // first key (multiple of kBlock)
+  int16_t n_rows;            // rows (context positions) in the item
+  int16_t part_stride;       // tiles: distance between the partial slots of consecutive rows
+  int32_t key_begin;         // first key (row items: multiple of kBlock; tiles: of kKeyTile)
   int32_t key_end;           // one past the last key any row reads
   int32_t pos0;              // context position of the first row
   int32_t bt_off;            // offset of the request's block table in block_ids
-  int32_t part;              // row items: partial slot, -1 = write O directly
+  int32_t part;              // partial slot of the first row, -1 = write O directly
 };
 
 struct MergeGroup {          // 16 bytes
@@ -54,9 +58,10 @@ static_assert(sizeof(WorkItem) == 32, "work item layout");
 static_assert(sizeof(MergeGroup) == 16, "merge group layout");
 
 // Split-K partial of one (row, KV head, key span): unnormalised o[G][D]
-// relative to the running maximum, then m[G] (log2 domain) and l[G].
+// relative to the running maximum, then m[G] (log2 domain) and l[G], padded to
+// a multiple of 4 floats so every slot starts 16-byte aligned.
 constexpr int64_t partial_floats(int32_t group, int32_t head_dim) {
-  return static_cast<int64_t>(group) * (head_dim + 2);
+  return ((static_cast<int64_t>(group) * (head_dim + 2) + 3) / 4) * 4;
 }
 
 }  // namespace aug

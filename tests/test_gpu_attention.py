@@ -50,6 +50,8 @@ CASES = [
     ([1, 9, 1], [513, 100, 48], 16, 4, 64, "bf16"),                          # D=64 tiles
     ([1, 3, 1, 1], [400, 40, 1, 77], 64, 8, 128, "fp8"),                     # fp8 KV (row path)
     ([2, 1, 1], [35, 250, 16], 8, 2, 128, "f32"),                            # f32 D=128, G=4
+    ([70, 1, 5], [2600, 1500, 2100], 32, 8, 128, "bf16"),                    # split tiles (3 spans)
+    ([20, 130], [1100, 2200], 16, 2, 64, "bf16"),                            # split tiles, D=64, G=8
 ]
 
 
