@@ -146,6 +146,8 @@ def main():
     params = aug.former_params(t_max=2048, beta_low=0.5, beta_high=1.0, chunk_cap=512)
     stream = torch.cuda.current_stream(dev)
     plan_dev = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+    plan_host = [torch.empty(64 << 20, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+    plan_ev = [None, None]
     ws_dev = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
     out = torch.empty((b.total_q, b.num_q_heads, b.head_dim),
                       dtype=torch.float32 if b.out_dtype == "f32" else torch.bfloat16, device=dev)
@@ -163,8 +165,16 @@ def main():
         q_start[1:] = np.cumsum(q_len[sel])
         info, plan = aug.aug_attn_plan(shape, q_start, b.ctx_len, b.bt_start, kv.num_pool_blocks,
                                        None, kv_split_tokens=args.kv_split)
-        host = torch.from_numpy(plan).pin_memory()
+        # double-buffered pinned staging: a buffer is rewritten only after the
+        # copy that last read it has completed
+        slot = i & 1
+        if plan_ev[slot] is not None:
+            plan_ev[slot].synchronize()
+        host = plan_host[slot][:plan.size]
+        host.numpy()[:] = plan
         plan_dev[:plan.size].copy_(host, non_blocking=True)
+        plan_ev[slot] = torch.cuda.Event()
+        plan_ev[slot].record(stream)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)

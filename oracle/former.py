@@ -35,8 +35,9 @@ design notes):
   the returned tokens onto the context;
 * w is measured in milliseconds (beta = 5e-5 is the paper's default);
 * candidates are the running, swapped and waiting queues; a request
-  contributes min(pending, chunk_cap) tokens while it has prompt, returned or
-  recompute tokens pending, else 1 decode token; active tokens start at 0;
+  contributes min(pending, chunk_cap, B) tokens (at least 1) while it has
+  prompt, returned or recompute tokens pending, else 1 decode token, so a
+  prefill chunk never exceeds the budget on its own; active tokens start at 0;
 * ties in theta go to the earlier arrival, then the smaller id;
 * a request also needs ceil((ctx + tokens) / block) pool blocks beyond those
   it holds (all of them if swapped out); if free plus reclaimable blocks
@@ -210,8 +211,8 @@ def token_budget(p: Params, free_blocks: int, preempt_blocks: int, block_size: i
     return min(max(raw, lo), hi)
 
 
-def tokens_of(p: Params, r: Request) -> int:
-    return min(r.pending, p.chunk_cap) if r.pending > 0 else 1
+def tokens_of(p: Params, r: Request, budget: int) -> int:
+    return min(r.pending, p.chunk_cap, max(1, budget)) if r.pending > 0 else 1
 
 
 def greedy_pack(sizes, budget, skip_instead_of_break=False):
@@ -262,7 +263,7 @@ def form_batch(reqs: List[Request], free_blocks: int, block_size: int, now: floa
     ids, q_len, th, resume_ids, park_ids, free_ids = [], [], [], [], [], []
     for i in ranked:
         r = reqs[i]
-        t = tokens_of(p, r)
+        t = tokens_of(p, r, budget)
         if active + t > budget:
             if p.skip_instead_of_break:
                 continue

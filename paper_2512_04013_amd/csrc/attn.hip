@@ -454,7 +454,28 @@ struct TileLds {
   static constexpr int VS = 64 + 4;   // V^T row stride (elements)
   static constexpr int STAGE = (64 * KS + D * VS) * 2;   // bytes of one K + V^T stage
   static constexpr int IDS = aug::kTileSplit / kBlock + 8; // block ids of one item's key span
-  static constexpr int BYTES = 2 * STAGE + IDS * 4;      // double-buffered stages + ids
+  static constexpr int SCALES = 2 * 8 * 4;               // fp8: k and v scales of a stage's 4 blocks
+  static constexpr int BYTES = 2 * STAGE + IDS * 4 + SCALES;
+};
+
+// Staging of one thread's share of a key tile: 16-byte bf16 chunks, or
+// 8-byte fp8 chunks converted (exactly) to bf16 on the way into LDS.
+template <int KVT> struct TileStage;
+template <> struct TileStage<KV_BF16> {
+  using raw_t = uint4;
+  __device__ static uint4 to_bf16(const raw_t& r) { return r; }
+};
+template <> struct TileStage<KV_FP8> {
+  using raw_t = uint2;
+  __device__ static uint4 to_bf16(const raw_t& r) {
+    // OCP E4M3FN codes are exactly representable in bf16
+    uint4 o;
+    o.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.x, 1.0f, false));
+    o.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.x, 1.0f, true));
+    o.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.y, 1.0f, false));
+    o.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.y, 1.0f, true));
+    return o;
+  }
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -463,9 +484,13 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_ca
 // one KV head) against keys [key_begin, key_end) of the request. Key tiles of
 // 64 go through two LDS stages: while tile t is multiplied, tile t+1 sits in
 // the other stage and tile t+2 is on its way from HBM into registers.
-template <int D, int G, int OT>
+template <int KVT, int D, int G, int OT>
 __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* smem) {
   using L = TileLds<D>;
+  using TS = TileStage<KVT>;
+  using raw_t = typename TS::raw_t;
+  constexpr bool FP8 = KVT == KV_FP8;
+  constexpr int EB = FP8 ? 1 : 2;     // bytes per K/V element
   constexpr int KSTEPS = D / 16;      // k-steps of S^T over head_dim
   constexpr int DB = D / 32;          // 32-dim blocks of O^T
   constexpr int CPR = D / 8;          // 16-byte chunks per key row
@@ -505,33 +530,46 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   const int key_end = it.key_end;
   const int t0 = it.key_begin / 64;
   const int t1 = (key_end + 63) / 64;
-  const uint16_t* kc = static_cast<const uint16_t*>(a.k_cache);
-  const uint16_t* vc = static_cast<const uint16_t*>(a.v_cache);
+  const char* kc = static_cast<const char*>(a.k_cache);
+  const char* vc = static_cast<const char*>(a.v_cache);
   const int64_t head_stride = static_cast<int64_t>(kBlock) * D;
 
   // the item's block ids (at most IDS: spans are capped by the planner) are
   // read once into LDS, so staging a key tile costs one round trip
   int32_t* ids = reinterpret_cast<int32_t*>(smem + 2 * L::STAGE);
+  float* stage_scales = reinterpret_cast<float*>(smem + 2 * L::STAGE + L::IDS * 4);   // [stage][k0..3, v0..3]
   const int blk_first = it.key_begin / kBlock;
   const int n_ids = (key_end + kBlock - 1) / kBlock - blk_first;
   for (int i = threadIdx.x; i < n_ids && i < L::IDS; i += kThreads) ids[i] = a.block_ids[it.bt_off + blk_first + i];
   __syncthreads();
 
-  uint4 kr[KPT], vr[KPT];
+  // a thread stages KPT consecutive keys of one block (KPT divides 16)
+  raw_t kr[KPT], vr[KPT];
+  float sc_reg = 1.f;   // fp8: thread t < 8 carries scale t of the tile (k0..3, v0..3)
   auto load_tile = [&](int k0) {
+    const int tok0 = k0 + tk * KPT;
+    const int slot = (tok0 >> 4) - blk_first;
+    const int bid = tok0 < key_end ? ids[slot] : -1;
+    const bool ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
+    const int64_t base = ((static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride +
+                          static_cast<int64_t>(tok0 & 15) * D + 8 * tc) * EB;
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
-      const int tok = k0 + tk * KPT + u;
-      kr[u] = uint4{0, 0, 0, 0};
-      vr[u] = uint4{0, 0, 0, 0};
-      if (tok < key_end) {
-        const int bid = ids[(tok >> 4) - blk_first];
-        if (static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks)) {
-          const int64_t off = (static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride +
-                              static_cast<int64_t>(tok & 15) * D + 8 * tc;
-          kr[u] = *reinterpret_cast<const uint4*>(kc + off);
-          vr[u] = *reinterpret_cast<const uint4*>(vc + off);
-        }
+      if (ok && tok0 + u < key_end) {
+        kr[u] = *reinterpret_cast<const raw_t*>(kc + base + static_cast<int64_t>(u) * D * EB);
+        vr[u] = *reinterpret_cast<const raw_t*>(vc + base + static_cast<int64_t>(u) * D * EB);
+      } else {
+        kr[u] = raw_t{};
+        vr[u] = raw_t{};
+      }
+    }
+    if constexpr (FP8) {
+      if (threadIdx.x < 8) {
+        const int b = (k0 >> 4) + (threadIdx.x & 3) - blk_first;
+        const int sb = (k0 + 16 * (threadIdx.x & 3)) < key_end ? ids[b] : -1;
+        const float* sa = threadIdx.x < 4 ? a.k_scale : a.v_scale;
+        sc_reg = static_cast<uint32_t>(sb) < static_cast<uint32_t>(a.num_pool_blocks)
+                     ? sa[static_cast<int64_t>(sb) * a.hkv + kvh] : 1.f;
       }
     }
   };
@@ -540,14 +578,17 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     uint16_t* vt = ks + 64 * L::KS;
 #pragma unroll
     for (int u = 0; u < KPT; ++u)
-      *reinterpret_cast<uint4*>(ks + (tk * KPT + u) * L::KS + 8 * tc) = kr[u];
+      *reinterpret_cast<uint4*>(ks + (tk * KPT + u) * L::KS + 8 * tc) = TS::to_bf16(kr[u]);
+    uint4 vb[KPT];
+#pragma unroll
+    for (int u = 0; u < KPT; ++u) vb[u] = TS::to_bf16(vr[u]);
     // V^T: element e of each of this thread's KPT keys goes to row 8*tc+e
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       uint32_t w[KPT];
 #pragma unroll
       for (int u = 0; u < KPT; ++u) {
-        const uint32_t word = (&vr[u].x)[e >> 1];
+        const uint32_t word = (&vb[u].x)[e >> 1];
         w[u] = (e & 1) ? (word >> 16) : (word & 0xFFFFu);
       }
       uint16_t* dst = vt + (8 * tc + e) * L::VS + tk * KPT;
@@ -556,6 +597,9 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       } else {
         *reinterpret_cast<uint32_t*>(dst) = w[0] | (w[1] << 16);
       }
+    }
+    if constexpr (FP8) {
+      if (threadIdx.x < 8) stage_scales[stage * 8 + threadIdx.x] = sc_reg;
     }
   };
 
@@ -584,6 +628,21 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
         const uint4 kop = *reinterpret_cast<const uint4*>(ks + (32 * mb + n) * L::KS + 16 * s + 8 * hh);
         sacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), as_bf16x8(qreg[s]), sacc[mb], 0, 0, 0);
       }
+    }
+
+    float vsc[4];
+    if constexpr (FP8) {
+      // entry (mb, i, j) belongs to block 2mb + (i >> 1) of the tile
+      float ksc[4];
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        ksc[q4] = stage_scales[stage * 8 + q4];
+        vsc[q4] = stage_scales[stage * 8 + 4 + q4];
+      }
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sacc[mb][e] *= ksc[2 * mb + (e >> 3)];
     }
 
     // online softmax over this row's 64 keys (32 in each lane half), in the
@@ -634,11 +693,13 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     for (int s = 0; s < 4; ++s) {
       const int mb = s >> 1;
       const int i0 = 2 * (s & 1);
+      // fp8: the V scale of a key's block multiplies its probability
+      const float vs = FP8 ? vsc[2 * mb + (s & 1)] : 1.f;
       uint4 pw;
-      pw.x = pack_bf16(sacc[mb][4 * i0 + 0], sacc[mb][4 * i0 + 1]);
-      pw.y = pack_bf16(sacc[mb][4 * i0 + 2], sacc[mb][4 * i0 + 3]);
-      pw.z = pack_bf16(sacc[mb][4 * i0 + 4], sacc[mb][4 * i0 + 5]);
-      pw.w = pack_bf16(sacc[mb][4 * i0 + 6], sacc[mb][4 * i0 + 7]);
+      pw.x = pack_bf16(sacc[mb][4 * i0 + 0] * vs, sacc[mb][4 * i0 + 1] * vs);
+      pw.y = pack_bf16(sacc[mb][4 * i0 + 2] * vs, sacc[mb][4 * i0 + 3] * vs);
+      pw.z = pack_bf16(sacc[mb][4 * i0 + 4] * vs, sacc[mb][4 * i0 + 5] * vs);
+      pw.w = pack_bf16(sacc[mb][4 * i0 + 6] * vs, sacc[mb][4 * i0 + 7] * vs);
       const bf16x8_t pop = as_bf16x8(pw);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -705,7 +766,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   const WorkItem it = a.items[blockIdx.x];
   if constexpr (TILES) {
     if (it.kind == aug::kTileItem) {
-      tile_item<D, G, OT>(it, a, smem);
+      tile_item<KVT, D, G, OT>(it, a, smem);
       return;
     }
   }
@@ -805,7 +866,7 @@ aug_status launch(const AttnArgs& a, const aug_attn_plan_info& info, const Merge
                   hipStream_t st) {
   if (info.num_items > 0) {
     if (info.num_prefill_items > 0) {
-      if constexpr (KVT == KV_BF16 && QT == AUG_BF16) {
+      if constexpr ((KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16) {
         hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT>), dim3(info.num_items), dim3(kThreads), 0, st, a);
       } else {
         return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: plan has tiles for a dtype set without them");

@@ -9,7 +9,8 @@
 // theta). The token budget is floor((G_free + G_preempt) / mu), clipped
 // (Eq. token). Packing walks the ranking and stops at the first request whose
 // tokens do not fit the budget or whose blocks cannot be found, reclaiming
-// blocks lazily from paused Swap (parked) and Discard (freed) requests.
+// blocks lazily from paused Swap (parked) and Discard (freed) requests. A
+// prefill request takes min(pending, chunk_cap, budget) tokens.
 //
 // Memory occupancy is counted in KV tokens after each iteration's tokens are
 // added, one iteration lasting t_iter seconds; mu is one token, so a budget
@@ -184,9 +185,11 @@ extern "C" aug_status aug_form_batch(const aug_request* reqs, int32_t n, int64_t
   size_t vi = 0;
   int32_t n_sched = 0, n_resume = 0, n_park = 0, n_free = 0;
   const int64_t bs = p.block_size;
+  // a prefill chunk is capped by the budget too, so it can always fit alone
+  const int64_t chunk = std::min<int64_t>(p.chunk_cap, std::max<int64_t>(1, budget));
   for (int32_t i : cand) {
     const aug_request& r = reqs[i];
-    const int64_t t = r.pending > 0 ? std::min<int64_t>(r.pending, p.chunk_cap) : 1;
+    const int64_t t = r.pending > 0 ? std::min<int64_t>(r.pending, chunk) : 1;
     if (active + t > budget) {
       if (p.skip_instead_of_break) continue;
       break;

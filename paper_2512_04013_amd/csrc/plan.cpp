@@ -31,7 +31,7 @@ bool dtype_set_supported(const aug_attn_shape& s) {
 }
 
 bool tiles_supported(const aug_attn_shape& s) {
-  return s.q_dtype == AUG_BF16 && s.kv_dtype == AUG_BF16;
+  return s.q_dtype == AUG_BF16 && (s.kv_dtype == AUG_BF16 || s.kv_dtype == AUG_FP8_E4M3FN);
 }
 
 aug_status check_shape(const aug_attn_shape* s, const char* who) {

@@ -4,8 +4,8 @@ import sys
 
 import numpy as np
 
-# Tolerances. bf16 I/O with fp32 accumulation: max-abs 1e-2 and mean-abs
-# 1e-3 against the float64 oracle, plus a per-row relative L2 bound that a
+# Tolerances. bf16 I/O with fp32 accumulation: max-abs 1e-2 (relative to
+# |o| where |o| > 1) and mean-abs 1e-3 against the float64 oracle, plus a per-row relative L2 bound that a
 # kernel dropping a whole block cannot meet on near-uniform attention. fp32
 # I/O: the only error sources are fp32 rounding and the hardware exp2, so the
 # bounds are far tighter.
@@ -28,7 +28,12 @@ def compare(got: np.ndarray, want: np.ndarray, out_dtype: str, rows=None, what="
     assert np.isfinite(got).all(), f"{what}: non-finite outputs"
     tol = TOL[out_dtype]
     diff = np.abs(got - want)
-    max_abs, mean_abs = float(diff.max()), float(diff.mean())
+    # The max-abs gate holds for outputs of magnitude up to 1 (the configured
+    # workloads' outputs are far smaller). Above 1 it scales with |o|: a bf16
+    # output in [4, 8) alone carries up to half an ulp = 2^-6 of rounding, so a
+    # fixed 1e-2 could not be met by any bf16 kernel on the sharp inputs.
+    max_abs = float((diff / np.maximum(1.0, np.abs(want))).max())
+    mean_abs = float(diff.mean())
     num = np.sqrt(((got - want) ** 2).sum(axis=-1))
     den = np.sqrt((want ** 2).sum(axis=-1))
     rel = float((num / np.maximum(den, 1e-6)).max())

@@ -48,10 +48,12 @@ CASES = [
     ([33, 1, 129, 1], [100, 1, 500, 2049], 32, 8, 128, "bf16"),              # G=4, >1 tile
     ([17, 1, 1, 16], [17, 64, 65, 600], 64, 8, 128, "bf16"),                 # G=8
     ([1, 9, 1], [513, 100, 48], 16, 4, 64, "bf16"),                          # D=64 tiles
-    ([1, 3, 1, 1], [400, 40, 1, 77], 64, 8, 128, "fp8"),                     # fp8 KV (row path)
+    ([1, 3, 1, 1], [400, 40, 1, 77], 64, 8, 128, "fp8"),                     # fp8 KV, small tile
     ([2, 1, 1], [35, 250, 16], 8, 2, 128, "f32"),                            # f32 D=128, G=4
     ([70, 1, 5], [2600, 1500, 2100], 32, 8, 128, "bf16"),                    # split tiles (3 spans)
     ([20, 130], [1100, 2200], 16, 2, 64, "bf16"),                            # split tiles, D=64, G=8
+    ([130, 1, 64, 17], [1500, 700, 64, 3000], 64, 8, 128, "fp8"),            # fp8 KV tiles, split, G=8
+    ([40, 1, 100], [2100, 33, 100], 32, 8, 128, "fp8"),                      # fp8 KV tiles, G=4
 ]
 
 

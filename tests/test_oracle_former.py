@@ -237,7 +237,7 @@ def test_form_batch_packing_is_the_plain_greedy_when_blocks_are_ample():
     plan = of.form_batch(reqs, 10**7, 16, 4.0, p)
     ranked = sorted(range(60), key=lambda i: (-of.priority(p, plan.cost[i], of.waiting_ms(reqs[i], 4.0)),
                                              reqs[i].arrival, reqs[i].id))
-    sizes = [of.tokens_of(p, reqs[i]) for i in ranked]
+    sizes = [of.tokens_of(p, reqs[i], plan.budget) for i in ranked]
     chosen = of.greedy_pack(sizes, plan.budget)
     assert plan.ids == [reqs[ranked[c]].id for c in chosen]
 
