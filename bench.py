@@ -57,6 +57,26 @@ def prefill_flops(b) -> float:
     return float(4 * b.head_dim * b.num_q_heads * keys.sum())
 
 
+def measured_traffic(workload_name: str):
+    """HBM bytes per attention call from the committed rocprofv3 counter
+    summary, or None when the summary does not cover this workload or the
+    kernel and planner sources have changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    h = hashlib.sha256()
+    for name in rec.get("source_files", []):
+        with open(os.path.join(ROOT, name), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec.get("source_sha256"):
+        return None
+    w = rec.get("workloads", {}).get(workload_name)
+    return None if w is None else int(w["bytes_per_call"])
+
+
 def request_records(b, aug):
     """Scheduler view of the batch: prefill chunks as waiting requests with
     pending tokens, decodes as running requests."""
@@ -215,7 +235,7 @@ def main():
     flops = prefill_flops(b)
     achieved_gbs = nbytes / (attn_ms * 1e-3) / 1e9
     roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(b.name),
             "kernel": "aug_attn_mixed launches (attention + split-K merge)",
             "algorithmic_bytes_per_launch": int(nbytes), "launch_ms": round(attn_ms, 4)}
     if flops > 0:
