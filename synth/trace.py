@@ -96,6 +96,7 @@ class SimConfig:
     per_context_token: float = 20.5e-9
     pred_err: float = 0.2
     max_iters: int = 10 ** 7
+    max_preemptions: int = 100_000   # recompute preemptions before the loop gives up (thrashing)
 
 
 @dataclasses.dataclass
@@ -128,6 +129,7 @@ class ServingLoop:
         self.first_token: Dict[int, float] = {}
         self.steps: List[StepRecord] = []
         self.preemptions = 0
+        self.last_ids = set()                                   # requests of the last non-empty iteration
 
     # ---- segment bookkeeping ------------------------------------------------------
 
@@ -274,17 +276,26 @@ class ServingLoop:
             if t is None:
                 # Nothing fits and no pause or arrival will change that: every
                 # block is held by runnable requests. Like an engine preempting by
-                # recomputation, drop the KV of the latest-arriving holder.
+                # recomputation, drop the KV of the latest-arriving holder, sparing
+                # the requests that ran in the previous iteration (so a request is
+                # never dropped right after it was given blocks) unless no other
+                # holder is left.
                 holders = [lv for lv in self.live.values()
                            if lv.rec["state"] in (RUNNING, SWAPPED, WAITING) and lv.rec["blocks_on_gpu"] > 0]
                 if not holders:
                     raise RuntimeError("serving loop cannot make progress (a request exceeds the pool)")
-                v = max(holders, key=lambda lv: (lv.tr.arrival, lv.tr.id))
+                idle = [lv for lv in holders if lv.tr.id not in self.last_ids]
+                v = max(idle or holders, key=lambda lv: (lv.tr.arrival, lv.tr.id))
                 self.free += v.rec["blocks_on_gpu"]
                 v.rec.update(state=WAITING, blocks_on_gpu=0, ctx_len=0, pending=v.logical_ctx + v.rec["pending"])
                 self.preemptions += 1
+                if self.preemptions > self.cfg.max_preemptions:
+                    raise RuntimeError("serving loop is thrashing: the pool is far smaller than the "
+                                       "contexts the scheduled requests need")
                 t = end
             self.now = max(end, t)
+        if ids:
+            self.last_ids = set(ids)
         self.steps.append(rec)
         return rec
 
