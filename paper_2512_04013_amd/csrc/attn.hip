@@ -17,7 +17,8 @@
 //    the vector ALUs in fp32.
 //  * Tile items (bf16 chunked prefill): 128 query rows (positions x group
 //    heads) of one chunk, causal against keys 0 .. last row's position. K and V
-//    are staged through LDS 64 keys at a time (V transposed on the way in), and
+//    are staged through LDS 64 keys at a time (V read back through transposing
+//    LDS loads), and
 //    both products run on bf16 MFMA 32x32x16 with fp32 accumulation:
 //    S^T = K Q^T puts one query row per lane column, so the row max/sum are
 //    lane-local plus one exchange between the two lane halves, and
@@ -55,6 +56,12 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
+// A running maximum is only moved (and the running sums rescaled) when a new
+// score exceeds it by more than this many powers of two; until then
+// probabilities are taken against the stale maximum and stay below 2^8, which
+// fp32 sums and bf16 probabilities carry without loss. Numerator and
+// denominator always share one reference, so the result is unchanged.
+constexpr float kRescaleSlack = 8.0f;
 constexpr int kThreads = 256;
 
 enum : int { KV_F32 = 0, KV_BF16 = 1, KV_FP8 = 2 };
@@ -352,9 +359,9 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
 #pragma unroll
       for (int i = 1; i < NLD; ++i) mb = fmaxf(mb, s[i][h]);
       mn[h] = fmaxf(m[h], mb);
-      moved |= mn[h] != m[h];
+      moved |= mn[h] > m[h] + kRescaleSlack;
     }
-    // rescale only when some running maximum moved (alpha is exactly 1 otherwise)
+    // rescale only when some running maximum moved far (see kRescaleSlack)
     if (__any(moved)) {
 #pragma unroll
       for (int h = 0; h < G; ++h) {
@@ -451,9 +458,11 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
 template <int D>
 struct TileLds {
   static constexpr int KS = D + 8;    // K row stride (elements): 16-byte aligned, conflict-free reads
-  static constexpr int VS = 64 + 4;   // V^T row stride (elements)
-  static constexpr int STAGE = (64 * KS + D * VS) * 2;   // bytes of one K + V^T stage
-  static constexpr int IDS = aug::kTileSplit / kBlock + 8; // block ids of one item's key span
+  // V row stride (elements): rows 64 bytes apart modulo the 256-byte bank
+  // width, so the transposing reads of four consecutive rows hit distinct banks
+  static constexpr int VS = D + 32;
+  static constexpr int STAGE = 64 * (KS + VS) * 2;       // bytes of one K + V stage
+  static constexpr int IDS = aug::kTileSpanMax / kBlock + 8; // block ids of one item's key span
   static constexpr int SCALES = 2 * 8 * 4;               // fp8: k and v scales of a stage's 4 blocks
   static constexpr int BYTES = 2 * STAGE + IDS * 4 + SCALES;
 };
@@ -479,6 +488,14 @@ template <> struct TileStage<KV_FP8> {
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef bf16x4_t __attribute__((address_space(3))) lds_bf16x4_t;
+
+// ds_read_b64_tr_b16: 8 bytes per lane, transposed across each 16-lane group
+__device__ __forceinline__ uint2 ds_read_tr16(const uint16_t* p) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p)));
+}
 
 // One tile item: up to 128 query rows (kTileRows / G positions x G heads of
 // one KV head) against keys [key_begin, key_end) of the request. Key tiles of
@@ -508,6 +525,9 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   const bool row_ok = p < it.n_rows;
   const int pos = it.pos0 + p;
   const uint16_t* qb = static_cast<const uint16_t*>(a.q);
+  // lane (dimension m = lane % 32, k-slot half hh) reads keys 4hh + {0..3}
+  // (and +8) of a 16-key step at dimension m of a 32-dim block
+  const int v_lane_off = (4 * hh + (lane & 15) / 4) * L::VS + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
   uint4 qreg[KSTEPS];
   {
@@ -575,28 +595,11 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   };
   auto store_tile = [&](int stage) {
     uint16_t* ks = reinterpret_cast<uint16_t*>(smem + stage * L::STAGE);
-    uint16_t* vt = ks + 64 * L::KS;
+    uint16_t* vs = ks + 64 * L::KS;
 #pragma unroll
-    for (int u = 0; u < KPT; ++u)
+    for (int u = 0; u < KPT; ++u) {
       *reinterpret_cast<uint4*>(ks + (tk * KPT + u) * L::KS + 8 * tc) = TS::to_bf16(kr[u]);
-    uint4 vb[KPT];
-#pragma unroll
-    for (int u = 0; u < KPT; ++u) vb[u] = TS::to_bf16(vr[u]);
-    // V^T: element e of each of this thread's KPT keys goes to row 8*tc+e
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      uint32_t w[KPT];
-#pragma unroll
-      for (int u = 0; u < KPT; ++u) {
-        const uint32_t word = (&vb[u].x)[e >> 1];
-        w[u] = (e & 1) ? (word >> 16) : (word & 0xFFFFu);
-      }
-      uint16_t* dst = vt + (8 * tc + e) * L::VS + tk * KPT;
-      if constexpr (KPT == 4) {
-        *reinterpret_cast<uint2*>(dst) = uint2{w[0] | (w[1] << 16), w[2] | (w[3] << 16)};
-      } else {
-        *reinterpret_cast<uint32_t*>(dst) = w[0] | (w[1] << 16);
-      }
+      *reinterpret_cast<uint4*>(vs + (tk * KPT + u) * L::VS + 8 * tc) = TS::to_bf16(vr[u]);
     }
     if constexpr (FP8) {
       if (threadIdx.x < 8) stage_scales[stage * 8 + threadIdx.x] = sc_reg;
@@ -615,20 +618,44 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       if (t + 2 < t1) load_tile(k0 + 128);
     }
     const uint16_t* ks = reinterpret_cast<const uint16_t*>(smem + stage * L::STAGE);
-    const uint16_t* vt = ks + 64 * L::KS;
+    const uint16_t* vs = ks + 64 * L::KS;
 
-    // S^T = K Q^T for keys k0..k0+63
+    // S^T = K Q^T for keys k0..k0+63. All K operands of the tile are read
+    // from LDS first, so the reads stream while the MFMAs consume them in order.
     f32x16_t sacc[2];
+    {
+      uint4 kop[2][KSTEPS];
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
+      for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[mb][e] = 0.f;
+        for (int s = 0; s < KSTEPS; ++s)
+          kop[mb][s] = *reinterpret_cast<const uint4*>(ks + (32 * mb + n) * L::KS + 16 * s + 8 * hh);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int s = 0; s < KSTEPS; ++s) {
-        const uint4 kop = *reinterpret_cast<const uint4*>(ks + (32 * mb + n) * L::KS + 16 * s + 8 * hh);
-        sacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop), as_bf16x8(qreg[s]), sacc[mb], 0, 0, 0);
+      for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sacc[mb][e] = 0.f;
+#pragma unroll
+        for (int s = 0; s < KSTEPS; ++s)
+          sacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kop[mb][s]), as_bf16x8(qreg[s]), sacc[mb], 0, 0, 0);
       }
     }
+    // V^T operands of the tile, read now so their latency hides behind the
+    // softmax. V sits row-major in LDS; the transposing LDS read gives lane i
+    // of a 16-lane group element (i % 4) of the 8-byte chunks addressed by
+    // lanes i/4, 4 + i/4, 8 + i/4 and 12 + i/4 of its group, so addressing
+    // row (lane % 16) / 4 at column 4 (lane % 4) hands each lane four
+    // consecutive keys of one dimension: the operand layout of V^T.
+    uint4 vop[4][DB];
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const uint16_t* v0 = vs + (16 * s) * L::VS + 32 * db + v_lane_off;
+        const uint2 lo = ds_read_tr16(v0);
+        const uint2 hi = ds_read_tr16(v0 + 8 * L::VS);
+        vop[s][db] = uint4{lo.x, lo.y, hi.x, hi.y};
+      }
 
     float vsc[4];
     if constexpr (FP8) {
@@ -648,7 +675,7 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     // online softmax over this row's 64 keys (32 in each lane half), in the
     // log2 domain: p = 2^(s*c - m). Keys past the row's position (or past
     // key_end) are masked. The running output is rescaled only when some
-    // row's maximum moved (the factor is exactly 1 otherwise).
+    // row's maximum moved by more than kRescaleSlack.
     const bool need_mask = k0 + 63 > it.pos0 || k0 + 64 > key_end;
     if (need_mask) {
       // entry (mb, i, j) of this lane is key k0 + 32mb + 8i + 4hh + j
@@ -668,7 +695,7 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       for (int e = (mb == 0 ? 1 : 0); e < 16; ++e) smax = fmaxf(smax, sacc[mb][e]);
     smax = fmaxf(smax, __shfl_xor(smax, 32));
     const float mn = fmaxf(m_run, smax * c);
-    if (__any(mn != m_run)) {
+    if (__any(mn > m_run + kRescaleSlack)) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
       l_run *= alpha;
 #pragma unroll
@@ -702,13 +729,8 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       pw.w = pack_bf16(sacc[mb][4 * i0 + 6] * vs, sacc[mb][4 * i0 + 7] * vs);
       const bf16x8_t pop = as_bf16x8(pw);
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const uint16_t* vrow = vt + (32 * db + n) * L::VS + 16 * s + 4 * hh;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
-        const uint4 vop{lo.x, lo.y, hi.x, hi.y};
-        acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vop), pop, acc_o[db], 0, 0, 0);
-      }
+      for (int db = 0; db < DB; ++db)
+        acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vop[s][db]), pop, acc_o[db], 0, 0, 0);
     }
   }
 

@@ -75,6 +75,20 @@ double row_item_ns(int64_t keys, int32_t head_dim, int32_t kv_bytes) {
 }
 double tile_item_ns(int64_t key_tiles) { return static_cast<double>(key_tiles) * 5000.0; }
 
+// Keys per span of a split prefill tile. Splitting costs a partial result
+// per row and span plus a merge, so tiles are split only as far as load
+// balance needs: no item should run much longer than the whole launch's work
+// spread over the resident workgroups (about two per compute unit).
+int32_t choose_tile_span(double total_ns) {
+  constexpr double kSlots = 512.0;
+  const double per_slot = total_ns / kSlots;
+  int64_t steps = static_cast<int64_t>(per_slot / tile_item_ns(1));
+  int64_t span = std::max<int64_t>(steps, 1) * kKeyTile;
+  span = std::max<int64_t>(span, kTileSpanMin);
+  span = std::min<int64_t>(span, kTileSpanMax);
+  return static_cast<int32_t>(span);
+}
+
 int32_t choose_split(int64_t total_row_keys, int32_t requested) {
   if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;
   // About four row items per compute unit (256 CUs) on small batches; on
@@ -139,6 +153,20 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
 
   const int32_t split = choose_split(total_row_keys, kv_split_tokens);
   const int32_t pos_per_tile = kTileRows / g;
+  const int32_t kv_bytes_all = s->kv_dtype == AUG_F32 ? 4 : s->kv_dtype == AUG_BF16 ? 2 : 1;
+
+  // estimated work of the whole launch, with every tile unsplit
+  double total_ns = static_cast<double>(total_row_keys) * s->head_dim * kv_bytes_all * 2 / 11.5;
+  for (int32_t r = 0; r < n; ++r) {
+    const int32_t q = b->q_start[r + 1] - b->q_start[r];
+    if (q <= 1 || !tiles_supported(*s)) continue;
+    const int32_t ctx = b->ctx_len[r];
+    for (int32_t j0 = 0; j0 < q; j0 += pos_per_tile) {
+      const int32_t key_end = ctx - q + j0 + std::min(pos_per_tile, q - j0);
+      total_ns += tile_item_ns((key_end + kKeyTile - 1) / kKeyTile) * hkv;
+    }
+  }
+  const int32_t tile_span = choose_tile_span(total_ns);
 
   // Row items: a request's spans are equal (within one block), so ordering
   // requests by span length orders their items longest first.
@@ -162,12 +190,13 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
         const int32_t key_end = pos0 + nr;
         // long tiles are split into near-equal spans of whole key tiles; each
         // row of a split tile then has one partial per span, stored together
-        const int32_t nsplit = (key_end + kTileSplit - 1) / kTileSplit;
+        const int32_t nsplit = (key_end + tile_span - 1) / tile_span;
         int32_t span = (key_end + nsplit - 1) / nsplit;
         span = ((span + kKeyTile - 1) / kKeyTile) * kKeyTile;
         const int32_t nsp = (key_end + span - 1) / span;
-        static_assert(kTileSplit % kKeyTile == 0, "tile spans are whole key tiles");
-        // span <= kTileSplit, so the kernel's per-item block-id buffer suffices
+        static_assert(kTileSpanMax % kKeyTile == 0 && kTileSpanMin % kKeyTile == 0,
+                      "tile spans are whole key tiles");
+        // span <= tile_span <= kTileSpanMax, so the kernel's per-item block-id buffer suffices
         for (int32_t h = 0; h < hkv; ++h) {
           for (int32_t sidx = 0; sidx < nsp; ++sidx) {
             WorkItem it{};
