@@ -102,3 +102,22 @@ def upload_batch(batch, device="cuda", staging_bytes=1 << 28):
     q = to_device_array(batch.q, batch.q_dtype, device)
     bids = torch.from_numpy(np.ascontiguousarray(batch.block_ids, dtype=np.int32)).to(device)
     return shape, kv, q, bids
+
+
+def serving_former(**params):
+    """A batch former for the serving loop (``synth.trace.ServingLoop``):
+    ``former(records, free_blocks, now)`` packs the records (dicts with the
+    request-record field names) into the library's request layout, calls
+    ``aug_form_batch`` and returns its plan dict. ``params`` are the fields of
+    the former's parameter record."""
+    from . import REQUEST_DTYPE, aug_form_batch, former_params
+    p = former_params(**params)
+    names = REQUEST_DTYPE.names
+
+    def run(recs, free_blocks, now):
+        arr = np.zeros(len(recs), REQUEST_DTYPE)
+        for k in names:
+            if k != "reserved":
+                arr[k] = [r[k] for r in recs]
+        return aug_form_batch(arr, free_blocks, now, p)
+    return run

@@ -8,6 +8,7 @@ import pytest
 
 import paper_2512_04013_amd as aug
 from oracle import former as of
+from synth import sweep
 from synth.trace import PAUSED, ServingLoop, SimConfig, make_trace
 from tests.former_drivers import library_former, lockstep, oracle_former
 
@@ -15,9 +16,7 @@ pytestmark = pytest.mark.skipif(not os.path.exists(aug.LIB_PATH), reason="libaug
 
 
 def params_for(budget, dynamic):
-    return of.Params(beta=5e-5, t_max=budget, beta_low=0.5 if dynamic else 1.0,
-                     beta_high=2.0 if dynamic else 1.0, chunk_cap=512, t_iter=0.02, fwd_a=0.0175,
-                     fwd_b=20.5e-9, swap_s_per_tok=4.1e-8, n_fwd_max=1)
+    return of.Params(**sweep.former_params(budget, dynamic))
 
 
 def small_trace(seed, n=60):
@@ -88,3 +87,34 @@ def test_lock_step_on_a_prefix_of_the_full_size_trace(budget):
     steps = loop.run(lockstep(oracle_former(p), library_former(p)), max_steps=400)
     assert len(steps) == 400
     assert all(sum(s.q_len) <= s.budget for s in steps)
+
+
+def test_serving_former_marshals_like_the_test_driver():
+    """The runtime's former callable (used by the benchmark and the GPU sweep)
+    returns the same plans as the test driver's, which is checked against the
+    oracle above; first 300 iterations of the full-size trace."""
+    from paper_2512_04013_amd import runtime as rt
+    p = sweep.former_params(1024)
+    product, driver = rt.serving_former(**p), library_former(of.Params(**p))
+
+    def both(recs, free, now):
+        a, b = product(recs, free, now), driver(recs, free, now)
+        for k in ("ids", "q_len", "resume_ids", "park_ids", "free_ids", "policy"):
+            assert list(a[k]) == list(b[k]), k
+        assert a["budget"] == b["budget"]
+        assert np.array_equal(np.asarray(a["theta"]).view(np.uint64), np.asarray(b["theta"]).view(np.uint64))
+        return a
+
+    loop = ServingLoop(make_trace(n=2000, seed=2), SimConfig(num_blocks=16384))
+    assert len(loop.run(both, max_steps=300)) == 300
+
+
+def test_sweep_budgets_from_512_serve_the_whole_trace():
+    """Every request of the 2000-request trace finishes under budget 512 with
+    the 16,384-block pool; budget 256 overloads it (the loop stops early)."""
+    from paper_2512_04013_amd import runtime as rt
+    run = sweep.run_budget(512, rt.serving_former(**sweep.former_params(512)))
+    assert run.complete and run.finished == 2000
+    assert all(sum(s.q_len) <= s.budget for s in run.steps)
+    small = sweep.run_budget(256, rt.serving_former(**sweep.former_params(256)), max_steps=2000)
+    assert not small.complete
