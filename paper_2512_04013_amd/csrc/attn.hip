@@ -36,6 +36,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "aug.h"
 #include "plan_format.h"
@@ -463,7 +464,10 @@ struct TileLds {
   static constexpr int VS = D + 32;
   static constexpr int STAGE = 64 * (KS + VS) * 2;       // bytes of one K + V stage
   static constexpr int IDS = aug::kTileSpanMax / kBlock + 8; // block ids of one item's key span
-  static constexpr int SCALES = 2 * 8 * 4;               // fp8: k and v scales of a stage's 4 blocks
+  // fp8, per stage and block of the tile: the K scale times the softmax
+  // coefficient, log2 of the V scale, and the V scale's reciprocal
+  static constexpr int NSC = 12;
+  static constexpr int SCALES = 2 * NSC * 4;
   static constexpr int BYTES = 2 * STAGE + IDS * 4 + SCALES;
 };
 
@@ -497,10 +501,29 @@ __device__ __forceinline__ uint2 ds_read_tr16(const uint16_t* p) {
   return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p)));
 }
 
+// v_permlane32_swap hands lane i the register of lane i + 32 (and back), so
+// combining both results pairs every lane with its partner in the other half.
+__device__ __forceinline__ float max_across_halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_across_halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+constexpr uint32_t kBf16PairOne = 0x3F803F80u;   // (1.0, 1.0) as packed bf16
+
+template <bool B> using bool_tag = std::integral_constant<bool, B>;
+
 // One tile item: up to 128 query rows (kTileRows / G positions x G heads of
 // one KV head) against keys [key_begin, key_end) of the request. Key tiles of
 // 64 go through two LDS stages: while tile t is multiplied, tile t+1 sits in
 // the other stage and tile t+2 is on its way from HBM into registers.
+//
+// Tiles that every row reads in full (all keys at or below the first row's
+// position and inside the span, all block ids inside the pool) take a path
+// without per-key conditions; only the diagonal and span-end tiles mask.
 template <int KVT, int D, int G, int OT>
 __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* smem) {
   using L = TileLds<D>;
@@ -557,30 +580,47 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   // the item's block ids (at most IDS: spans are capped by the planner) are
   // read once into LDS, so staging a key tile costs one round trip
   int32_t* ids = reinterpret_cast<int32_t*>(smem + 2 * L::STAGE);
-  float* stage_scales = reinterpret_cast<float*>(smem + 2 * L::STAGE + L::IDS * 4);   // [stage][k0..3, v0..3]
+  float* stage_scales = reinterpret_cast<float*>(smem + 2 * L::STAGE + L::IDS * 4);
   const int blk_first = it.key_begin / kBlock;
   const int n_ids = (key_end + kBlock - 1) / kBlock - blk_first;
-  for (int i = threadIdx.x; i < n_ids && i < L::IDS; i += kThreads) ids[i] = a.block_ids[it.bt_off + blk_first + i];
-  __syncthreads();
+  int bad = 0;
+  for (int i = threadIdx.x; i < n_ids && i < L::IDS; i += kThreads) {
+    const int32_t id = a.block_ids[it.bt_off + blk_first + i];
+    ids[i] = id;
+    bad |= static_cast<uint32_t>(id) >= static_cast<uint32_t>(a.num_pool_blocks);
+  }
+  bad = __syncthreads_or(bad);
+  const int t_full = bad ? t0 : max(t0, min(t1, min(it.pos0 + 1, key_end) / 64));
 
   // a thread stages KPT consecutive keys of one block (KPT divides 16)
   raw_t kr[KPT], vr[KPT];
   float sc_reg = 1.f;   // fp8: thread t < 8 carries scale t of the tile (k0..3, v0..3)
-  auto load_tile = [&](int k0) {
+  auto load_tile = [&](int k0, auto full_tag) {
+    constexpr bool FULL = decltype(full_tag)::value;
     const int tok0 = k0 + tk * KPT;
     const int slot = (tok0 >> 4) - blk_first;
-    const int bid = tok0 < key_end ? ids[slot] : -1;
-    const bool ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
-    const int64_t base = ((static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride +
-                          static_cast<int64_t>(tok0 & 15) * D + 8 * tc) * EB;
+    if constexpr (FULL) {
+      const int64_t base = ((static_cast<int64_t>(ids[slot]) * a.hkv + kvh) * head_stride +
+                            static_cast<int64_t>(tok0 & 15) * D + 8 * tc) * EB;
 #pragma unroll
-    for (int u = 0; u < KPT; ++u) {
-      if (ok && tok0 + u < key_end) {
+      for (int u = 0; u < KPT; ++u) {
         kr[u] = *reinterpret_cast<const raw_t*>(kc + base + static_cast<int64_t>(u) * D * EB);
         vr[u] = *reinterpret_cast<const raw_t*>(vc + base + static_cast<int64_t>(u) * D * EB);
-      } else {
-        kr[u] = raw_t{};
-        vr[u] = raw_t{};
+      }
+    } else {
+      const int bid = tok0 < key_end ? ids[slot] : -1;
+      const bool ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
+      const int64_t base = ((static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride +
+                            static_cast<int64_t>(tok0 & 15) * D + 8 * tc) * EB;
+#pragma unroll
+      for (int u = 0; u < KPT; ++u) {
+        if (ok && tok0 + u < key_end) {
+          kr[u] = *reinterpret_cast<const raw_t*>(kc + base + static_cast<int64_t>(u) * D * EB);
+          vr[u] = *reinterpret_cast<const raw_t*>(vc + base + static_cast<int64_t>(u) * D * EB);
+        } else {
+          kr[u] = raw_t{};
+          vr[u] = raw_t{};
+        }
       }
     }
     if constexpr (FP8) {
@@ -602,20 +642,32 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       *reinterpret_cast<uint4*>(vs + (tk * KPT + u) * L::VS + 8 * tc) = TS::to_bf16(vr[u]);
     }
     if constexpr (FP8) {
-      if (threadIdx.x < 8) stage_scales[stage * 8 + threadIdx.x] = sc_reg;
+      // K: the score coefficient of the block; V: its scale enters each
+      // probability as 2^(log2 vs) inside the exponential, and the row sum
+      // weighs the block by 1/vs. A zero scale (an all-zero block) is taken
+      // as 2^-100, which changes no result representable in fp32.
+      float* ss = stage_scales + stage * L::NSC;
+      if (threadIdx.x < 4) {
+        ss[threadIdx.x] = c * sc_reg;
+      } else if (threadIdx.x < 8) {
+        const float v = fmaxf(sc_reg, 0x1p-100f);
+        ss[threadIdx.x] = __builtin_amdgcn_logf(v);
+        ss[threadIdx.x + 4] = __builtin_amdgcn_rcpf(v);
+      }
     }
   };
 
-  load_tile(t0 * 64);
-  store_tile(0);
-  if (t0 + 1 < t1) load_tile((t0 + 1) * 64);
-  for (int t = t0; t < t1; ++t) {
+  auto step = [&](int t, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const int k0 = t * 64;
     const int stage = (t - t0) & 1;
     __syncthreads();   // stage `stage` is written; the other stage's readers are done
     if (t + 1 < t1) {
       store_tile(stage ^ 1);
-      if (t + 2 < t1) load_tile(k0 + 128);
+      if (t + 2 < t1) {
+        if (t + 2 < t_full) load_tile(k0 + 128, bool_tag<true>{});
+        else load_tile(k0 + 128, bool_tag<false>{});
+      }
     }
     const uint16_t* ks = reinterpret_cast<const uint16_t*>(smem + stage * L::STAGE);
     const uint16_t* vs = ks + 64 * L::KS;
@@ -657,44 +709,41 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
         vop[s][db] = uint4{lo.x, lo.y, hi.x, hi.y};
       }
 
-    float vsc[4];
-    if constexpr (FP8) {
-      // entry (mb, i, j) belongs to block 2mb + (i >> 1) of the tile
-      float ksc[4];
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        ksc[q4] = stage_scales[stage * 8 + q4];
-        vsc[q4] = stage_scales[stage * 8 + 4 + q4];
-      }
+    // Entry (mb, i, j) of this lane is key k0 + 32mb + 8i + 4hh + j, which
+    // lies in block b = 2mb + i/2 of the tile; b is also the PV step that
+    // consumes it. Keys past the row's position (or past key_end) are masked
+    // on boundary tiles.
+    const int lim = MASK ? min(pos, key_end - 1) - k0 - 4 * hh : 0;
+    auto live = [&](int mb, int e) { return !MASK || 32 * mb + 8 * (e >> 2) + (e & 3) <= lim; };
+    if constexpr (MASK) {
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) sacc[mb][e] *= ksc[2 * mb + (e >> 3)];
+        for (int e = 0; e < 16; ++e)
+          if (!live(mb, e)) sacc[mb][e] = -INFINITY;
     }
-
-    // online softmax over this row's 64 keys (32 in each lane half), in the
-    // log2 domain: p = 2^(s*c - m). Keys past the row's position (or past
-    // key_end) are masked. The running output is rescaled only when some
-    // row's maximum moved by more than kRescaleSlack.
-    const bool need_mask = k0 + 63 > it.pos0 || k0 + 64 > key_end;
-    if (need_mask) {
-      // entry (mb, i, j) of this lane is key k0 + 32mb + 8i + 4hh + j
-      const int lim = min(pos, key_end - 1) - k0 - 4 * hh;
+    // log2-domain coefficient of the raw score, per block (fp8: K scale folded in)
+    float coef[4], vlog[4], vinv[4];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (32 * mb + 8 * i + j > lim) sacc[mb][4 * i + j] = -INFINITY;
+    for (int b = 0; b < 4; ++b) {
+      coef[b] = FP8 ? stage_scales[stage * L::NSC + b] : c;
+      vlog[b] = FP8 ? stage_scales[stage * L::NSC + 4 + b] : 0.f;
+      vinv[b] = FP8 ? stage_scales[stage * L::NSC + 8 + b] : 1.f;
     }
-    float smax = sacc[0][0];
+    // row maximum of the scaled scores: block maxima of the raw scores times
+    // the (non-negative) block coefficients
+    float smax = -INFINITY;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int b = 0; b < 4; ++b) {
+      const int mb = b >> 1, e0 = 8 * (b & 1);
+      float bm = sacc[mb][e0];
 #pragma unroll
-      for (int e = (mb == 0 ? 1 : 0); e < 16; ++e) smax = fmaxf(smax, sacc[mb][e]);
-    smax = fmaxf(smax, __shfl_xor(smax, 32));
-    const float mn = fmaxf(m_run, smax * c);
+      for (int e = 1; e < 8; ++e) bm = fmaxf(bm, sacc[mb][e0 + e]);
+      smax = fmaxf(smax, FP8 ? bm * coef[b] : bm);
+    }
+    if constexpr (!FP8) smax *= c;
+    smax = max_across_halves(smax);
+    const float mn = fmaxf(m_run, smax);
     if (__any(mn > m_run + kRescaleSlack)) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
       l_run *= alpha;
@@ -704,37 +753,49 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
         for (int e = 0; e < 16; ++e) acc_o[db][e] *= alpha;
       m_run = mn;
     }
-    const float neg_m = -m_run;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[mb][e], c, neg_m));
-        sacc[mb][e] = pv;
-        l_run += pv;
-      }
 
-    // O^T += V^T P^T, 16 keys per step; k-slots of lane half hh are keys
-    // {16s+4hh+j, 16s+8+4hh+j}, exactly the S^T entries this lane holds
+    // p = 2^(s * coef - m) (fp8: times the block's V scale, through its log2),
+    // packed to bf16 pairs for the PV MFMAs; the row sum adds exactly the
+    // packed values (fp8: weighted back by 1/vs)
+    // O^T += V^T P^T, 16 keys (one block) per step; k-slots of lane half hh
+    // are keys {16s+4hh+j, 16s+8+4hh+j}, exactly the S^T entries this lane holds
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const int mb = s >> 1;
-      const int i0 = 2 * (s & 1);
-      // fp8: the V scale of a key's block multiplies its probability
-      const float vs = FP8 ? vsc[2 * mb + (s & 1)] : 1.f;
+      const int mb = s >> 1, e0 = 8 * (s & 1);
+      const float bias = vlog[s] - m_run;
+      float pv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = __builtin_amdgcn_exp2f(fmaf(sacc[mb][e0 + e], coef[s], bias));
+        pv[e] = live(mb, e0 + e) ? x : 0.f;
+      }
       uint4 pw;
-      pw.x = pack_bf16(sacc[mb][4 * i0 + 0] * vs, sacc[mb][4 * i0 + 1] * vs);
-      pw.y = pack_bf16(sacc[mb][4 * i0 + 2] * vs, sacc[mb][4 * i0 + 3] * vs);
-      pw.z = pack_bf16(sacc[mb][4 * i0 + 4] * vs, sacc[mb][4 * i0 + 5] * vs);
-      pw.w = pack_bf16(sacc[mb][4 * i0 + 6] * vs, sacc[mb][4 * i0 + 7] * vs);
+      pw.x = pack_bf16(pv[0], pv[1]);
+      pw.y = pack_bf16(pv[2], pv[3]);
+      pw.z = pack_bf16(pv[4], pv[5]);
+      pw.w = pack_bf16(pv[6], pv[7]);
+      const float bsum = dot2_bf16(pw.w, kBf16PairOne, dot2_bf16(pw.z, kBf16PairOne,
+                         dot2_bf16(pw.y, kBf16PairOne, dot2_bf16(pw.x, kBf16PairOne, 0.f))));
+      l_run = FP8 ? fmaf(bsum, vinv[s], l_run) : l_run + bsum;
       const bf16x8_t pop = as_bf16x8(pw);
 #pragma unroll
       for (int db = 0; db < DB; ++db)
         acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vop[s][db]), pop, acc_o[db], 0, 0, 0);
     }
-  }
+  };
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (t0 < t_full) load_tile(t0 * 64, bool_tag<true>{});
+  else load_tile(t0 * 64, bool_tag<false>{});
+  store_tile(0);
+  if (t0 + 1 < t1) {
+    if (t0 + 1 < t_full) load_tile((t0 + 1) * 64, bool_tag<true>{});
+    else load_tile((t0 + 1) * 64, bool_tag<false>{});
+  }
+  int t = t0;
+  for (; t < t_full; ++t) step(t, bool_tag<false>{});
+  for (; t < t1; ++t) step(t, bool_tag<true>{});
+
+  const float l_tot = sum_across_halves(l_run);
   if (!row_ok) return;
   if (it.part < 0) {
     const float inv = 1.f / l_tot;
