@@ -65,29 +65,25 @@ struct Sized {
 };
 
 // Estimated run time of a work item while the GPU is full (about 512
-// workgroups resident), used only to order items longest first so that
-// prefill tiles (compute bound) run beside decode spans (memory bound) and no
-// long item starts last. Calibrated on MI355X: a row item streams its K/V at
-// about 11.5 GB/s per resident workgroup (5.9 TB/s over 512), a 64-key MFMA
-// tile step of 128 rows takes about 5 us.
+// workgroups resident, two per compute unit), used to order items longest
+// first (so prefill tiles, compute bound, run beside decode spans, memory
+// bound, and no long item starts last) and to choose how far to split long
+// tiles. Calibrated on MI355X: a row item streams its K/V at about 11.5 GB/s
+// per resident workgroup (5.9 TB/s over 512); a tile item costs about 3 us
+// of set-up and write-out plus 2.6 us per 64-key step of its 128 rows; the
+// split-K merge launch about 5 us plus its partials read at 1.5 bytes/ns.
+constexpr int kSlots = 512;
 double row_item_ns(int64_t keys, int32_t head_dim, int32_t kv_bytes) {
   return static_cast<double>(keys) * head_dim * kv_bytes * 2 / 11.5;
 }
-double tile_item_ns(int64_t key_tiles) { return static_cast<double>(key_tiles) * 5000.0; }
-
-// Keys per span of a split prefill tile. Splitting costs a partial result
-// per row and span plus a merge, so tiles are split only as far as load
-// balance needs: no item should run much longer than the whole launch's work
-// spread over the resident workgroups (about two per compute unit).
-int32_t choose_tile_span(double total_ns) {
-  constexpr double kSlots = 512.0;
-  const double per_slot = total_ns / kSlots;
-  int64_t steps = static_cast<int64_t>(per_slot / tile_item_ns(1));
-  int64_t span = std::max<int64_t>(steps, 1) * kKeyTile;
-  span = std::max<int64_t>(span, kTileSpanMin);
-  span = std::min<int64_t>(span, kTileSpanMax);
-  return static_cast<int32_t>(span);
+double tile_item_ns(int64_t key_tiles) { return 3000.0 + static_cast<double>(key_tiles) * 2600.0; }
+double merge_ns(int64_t partial_bytes) {
+  return partial_bytes > 0 ? 5000.0 + static_cast<double>(partial_bytes) / 1.5 : 0.0;
 }
+
+// Lower bound of a launch's makespan on kSlots slots: its longest item, or
+// its total work spread evenly.
+double makespan_bound(double longest, double total) { return std::max(longest, total / kSlots); }
 
 int32_t choose_split(int64_t total_row_keys, int32_t requested) {
   if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;
@@ -155,18 +151,58 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   const int32_t pos_per_tile = kTileRows / g;
   const int32_t kv_bytes_all = s->kv_dtype == AUG_F32 ? 4 : s->kv_dtype == AUG_BF16 ? 2 : 1;
 
-  // estimated work of the whole launch, with every tile unsplit
-  double total_ns = static_cast<double>(total_row_keys) * s->head_dim * kv_bytes_all * 2 / 11.5;
-  for (int32_t r = 0; r < n; ++r) {
-    const int32_t q = b->q_start[r + 1] - b->q_start[r];
-    if (q <= 1 || !tiles_supported(*s)) continue;
-    const int32_t ctx = b->ctx_len[r];
-    for (int32_t j0 = 0; j0 < q; j0 += pos_per_tile) {
-      const int32_t key_end = ctx - q + j0 + std::min(pos_per_tile, q - j0);
-      total_ns += tile_item_ns((key_end + kKeyTile - 1) / kKeyTile) * hkv;
+  // Keys per span of a split prefill tile. Splitting evens out the items but
+  // costs a partial per row and span and their merge, so each candidate span
+  // is priced as the makespan of the whole launch (row items included) plus
+  // its merge, and the cheapest wins (ties: the longer span).
+  int32_t tile_span = kTileSpanMax;
+  int32_t longest_tile = 0;
+  for (int32_t r = 0; r < n && tiles_supported(*s); ++r)
+    if (b->q_start[r + 1] - b->q_start[r] > 1) longest_tile = std::max(longest_tile, b->ctx_len[r]);
+  if (longest_tile > kTileSpanMin) {
+    double row_total = 0.0, row_longest = 0.0;
+    int64_t row_partial_bytes = 0;
+    for (int32_t r = 0; r < n; ++r) {
+      const int32_t q = b->q_start[r + 1] - b->q_start[r];
+      if (q > 1) continue;
+      const int32_t ctx = b->ctx_len[r];
+      const int32_t nspan = (ctx + split - 1) / split;
+      const int32_t span = (((ctx + nspan - 1) / nspan + kBlock - 1) / kBlock) * kBlock;
+      const int32_t nsp = (ctx + span - 1) / span;
+      const double t = row_item_ns(std::min(span, ctx), s->head_dim, kv_bytes_all);
+      row_longest = std::max(row_longest, t);
+      row_total += row_item_ns(ctx, s->head_dim, kv_bytes_all) * hkv;
+      if (nsp > 1) row_partial_bytes += static_cast<int64_t>(nsp) * hkv * partial_floats(g, s->head_dim) * 4;
+    }
+    double best = 0.0;
+    bool have = false;
+    for (const int32_t cand : {kTileSpanMax, 4096, 2048, kTileSpanMin}) {
+      if (have && longest_tile <= cand) continue;   // nothing splits: same as the longer span
+      double total = row_total, longest = row_longest;
+      int64_t partial_bytes = row_partial_bytes;
+      for (int32_t r = 0; r < n; ++r) {
+        const int32_t q = b->q_start[r + 1] - b->q_start[r];
+        if (q <= 1) continue;
+        const int32_t ctx = b->ctx_len[r];
+        for (int32_t j0 = 0; j0 < q; j0 += pos_per_tile) {
+          const int32_t nr = std::min(pos_per_tile, q - j0);
+          const int32_t key_end = ctx - q + j0 + nr;
+          const int32_t nsplit = (key_end + cand - 1) / cand;
+          const int32_t span = (((key_end + nsplit - 1) / nsplit + kKeyTile - 1) / kKeyTile) * kKeyTile;
+          const int32_t nsp = (key_end + span - 1) / span;
+          longest = std::max(longest, tile_item_ns((std::min(span, key_end) + kKeyTile - 1) / kKeyTile));
+          total += (tile_item_ns(0) * nsp + tile_item_ns((key_end + kKeyTile - 1) / kKeyTile) - tile_item_ns(0)) * hkv;
+          if (nsp > 1) partial_bytes += static_cast<int64_t>(nr) * nsp * hkv * partial_floats(g, s->head_dim) * 4;
+        }
+      }
+      const double cost = makespan_bound(longest, total) + merge_ns(partial_bytes);
+      if (!have || cost < best) {
+        best = cost;
+        tile_span = cand;
+        have = true;
+      }
     }
   }
-  const int32_t tile_span = choose_tile_span(total_ns);
 
   // Row items: a request's spans are equal (within one block), so ordering
   // requests by span length orders their items longest first.
