@@ -40,6 +40,8 @@ WORKLOADS = {
     # under an 8192-token budget, on the 64/8-head fp8-KV layer
     "sweep-prefill-fp8": 5,   # the batch with the most prefill query-key pairs
     "sweep-context-fp8": 5,   # the batch with the most context tokens
+    # every budget 256 ... 8192: a sample of the formed batches replayed on one pool
+    "budget-sweep-fp8": 6,
 }
 
 
@@ -143,6 +145,136 @@ def make_workload(name: str, seed: int, log):
     return sweep.batch_for_step(run.steps[pick], seed=seed + 1000, name=f"{name}-budget{budget}"), budget
 
 
+def budget_sweep(args, log):
+    """Token-budget sweep: for each budget, serve the 2000-request trace with
+    the library's former, then replay a sample of the batches it formed (up
+    to --sweep-batches, evenly spaced over the run, plus its largest and most
+    prefill-heavy batch) through planner, upload and attention on one 16,384-
+    block fp8 pool of random codes and scales. Reports per budget and overall:
+    query tokens per second of the attention launches (HIP events) and of
+    whole replayed steps, and the fractions of the HBM and MFMA roofs."""
+    import torch
+    import paper_2512_04013_amd as aug
+    from paper_2512_04013_amd import runtime as rt
+    from synth import sweep
+
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(args.seed)
+    runs = {}
+    for budget in sweep.BUDGETS:
+        t0 = time.time()
+        run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), seed=args.seed,
+                               max_steps=4000 if budget == 256 else 40_000)
+        n = len(run.steps)
+        pick = sorted(set(np.linspace(0, n - 1, min(n, args.sweep_batches)).astype(int).tolist())
+                      | {sweep.select_steps(run.steps, 0, 0)[k] for k in ("most_tokens", "most_prefill")})
+        runs[budget] = (run, pick)
+        log(f"budget {budget}: {n} batches formed ({'whole trace' if run.complete else 'overloaded, stopped'}), "
+            f"{len(pick)} replayed ({time.time() - t0:.1f} s)")
+    hq, hkv, d = sweep.HEADS_Q, sweep.HEADS_KV, sweep.HEAD_DIM
+    nb = sweep.POOL_BLOCKS
+    gen = torch.Generator(device=dev).manual_seed(args.seed)
+    shape_kv = (nb, hkv, 16, d)
+    sign = torch.randint(0, 2, shape_kv, device=dev, dtype=torch.uint8, generator=gen) << 7
+    k_cache = torch.randint(0, 0x7F, shape_kv, device=dev, dtype=torch.uint8, generator=gen) | sign
+    sign = torch.randint(0, 2, shape_kv, device=dev, dtype=torch.uint8, generator=gen) << 7
+    v_cache = torch.randint(0, 0x7F, shape_kv, device=dev, dtype=torch.uint8, generator=gen) | sign
+    del sign
+    k_scale = torch.rand((nb, hkv), device=dev, generator=gen) * 1e-3 + 1e-4
+    v_scale = torch.rand((nb, hkv), device=dev, generator=gen) * 1e-3 + 1e-4
+    max_rows = max(sum(r.steps[i].q_len) for r, pick in runs.values() for i in pick)
+    q = torch.randn((max_rows, hq, d), device=dev, generator=gen).to(torch.bfloat16)
+    out = torch.empty((max_rows, hq, d), device=dev, dtype=torch.bfloat16)
+    shape = aug.make_shape(hq, hkv, d, "bf16", "fp8", "bf16", float(1.0 / np.sqrt(d)))
+    stream = torch.cuda.current_stream(dev)
+    plan_dev = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+    bid_dev = torch.empty(nb, dtype=torch.int32, device=dev)
+    ws_dev = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    host = [torch.empty(64 << 20, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+    host_ev = [None, None]
+
+    class B:   # the fields algorithmic_bytes / prefill_flops read
+        pass
+
+    results = {}
+    t_all, q_all, bytes_all, flops_all, wall_all = 0.0, 0, 0.0, 0.0, 0.0
+    for budget, (run, pick) in runs.items():
+        evs, qsum, nbytes, nflops = [], 0, 0.0, 0.0
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for k, i in enumerate(pick):
+            step = run.steps[i]
+            q_len = np.asarray(step.q_len, np.int32)
+            ctx = np.asarray(step.ctx_len, np.int32)
+            nblk = (ctx.astype(np.int64) + 15) // 16
+            q_start = np.zeros(len(q_len) + 1, np.int32)
+            q_start[1:] = np.cumsum(q_len)
+            bt_start = np.zeros(len(q_len) + 1, np.int32)
+            bt_start[1:] = np.cumsum(nblk)
+            bids = rng.permutation(nb)[:int(bt_start[-1])].astype(np.int32)
+            info, plan = aug.aug_attn_plan(shape, q_start, ctx, bt_start, nb, None)
+            slot = k & 1
+            if host_ev[slot] is not None:
+                host_ev[slot].synchronize()
+            hb = host[slot]
+            hb.numpy()[:plan.size] = plan
+            hb.numpy()[plan.size:plan.size + bids.nbytes] = bids.view(np.uint8)
+            plan_dev[:plan.size].copy_(hb[:plan.size], non_blocking=True)
+            bid_dev.view(torch.uint8)[:bids.nbytes].copy_(hb[plan.size:plan.size + bids.nbytes], non_blocking=True)
+            host_ev[slot] = torch.cuda.Event()
+            host_ev[slot].record(stream)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            aug.aug_attn_mixed(shape, info, plan_dev, q, k_cache, v_cache, k_scale, v_scale, bid_dev, nb, out,
+                               ws_dev, stream=stream.cuda_stream)
+            e1.record(stream)
+            evs.append((e0, e1))
+            b = B()
+            b.q_len, b.ctx_len, b.total_q = q_len, ctx, int(q_start[-1])
+            b.num_kv_heads, b.num_q_heads, b.head_dim = hkv, hq, d
+            b.kv_dtype, b.q_dtype, b.out_dtype = "fp8", "bf16", "bf16"
+            qsum += b.total_q
+            nbytes += algorithmic_bytes(b)
+            nflops += prefill_flops(b)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        t = sum(a.elapsed_time(c) for a, c in evs) * 1e-3
+        results[budget] = {"batches_formed": len(run.steps), "trace_complete": bool(run.complete),
+                           "batches_replayed": len(pick), "query_tokens": int(qsum),
+                           "attn_query_tokens_per_s": round(qsum / t, 1), "step_query_tokens_per_s": round(qsum / wall, 1),
+                           "hbm_frac": round(nbytes / t / (HBM_PEAK_GBS * 1e9), 4),
+                           "mfma_frac": round(nflops / t / (MFMA_BF16_PEAK_TFS * 1e12), 4),
+                           "attn_ms_per_batch": round(1e3 * t / len(pick), 4)}
+        log(f"budget {budget}: {results[budget]}")
+        t_all += t
+        wall_all += wall
+        q_all += qsum
+        bytes_all += nbytes
+        flops_all += nflops
+    achieved_gbs = bytes_all / t_all / 1e9
+    achieved_tfs = flops_all / t_all / 1e12
+    if flops_all / (MFMA_BF16_PEAK_TFS * 1e12) > bytes_all / (HBM_PEAK_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": round(achieved_tfs, 1), "peak": MFMA_BF16_PEAK_TFS, "unit": "TFLOP/s",
+                "frac": round(achieved_tfs / MFMA_BF16_PEAK_TFS, 4), "traffic": None}
+    else:
+        roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+    roof.update({"kernel": "aug_attn_mixed launches over all replayed batches",
+                 "prefill_mfma_tflops": round(achieved_tfs, 2), "hbm_gbs": round(achieved_gbs, 1)})
+    n_rep = sum(len(p) for _, p in runs.values())
+    result = {
+        "metric": "mixed-batch attn query-tokens/s + % peak HBM GB/s (decode) / % MFMA (prefill)",
+        "value": round(q_all / wall_all, 1), "unit": "query-tokens/s", "n_gpus": 1, "steps": n_rep, "warmup": 0,
+        "ms_per_step": round(1e3 * wall_all / n_rep, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16-q/fp8e4m3-kv", "data": "synthetic",
+        "config": {"workload": "budget-sweep-fp8", "trace_requests": 2000, "q_heads": hq, "kv_heads": hkv,
+                   "head_dim": d, "block_size": 16, "pool_blocks": nb, "seed": args.seed,
+                   "budgets": {str(k): v for k, v in results.items()}},
+        "roofline": roof,
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -153,6 +285,8 @@ def main():
     ap.add_argument("--kv-split", type=int, default=0, help="keys per decode work item (0: planner's choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--sweep-batches", type=int, default=200,
+                    help="budget-sweep-fp8: formed batches replayed per budget")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB a few times (a kernel of known "
                          "traffic for calibrating hardware byte counters)")
@@ -173,6 +307,9 @@ def main():
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
+    if args.workload == "budget-sweep-fp8":
+        budget_sweep(args, log)
+        return
     t0 = time.time()
     b, t_max = make_workload(args.workload, args.seed, log)
     log(f"workload {b.name}: {b.num_reqs} requests, {b.total_q} query rows, "

@@ -180,6 +180,8 @@ template <int KVT, int QT> struct RowMath;
 template <> struct RowMath<KV_BF16, AUG_BF16> {
   static constexpr int QW = 4;                 // packed bf16 pairs per lane (8 elements)
   using q_t = uint32_t;
+  using k_t = uint4;
+  __device__ static const uint4& prep(const uint4& k) { return k; }
   __device__ static void load(const void* q, int64_t off, q_t* dst) {
     const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(q) + off);
     dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
@@ -195,6 +197,8 @@ template <> struct RowMath<KV_BF16, AUG_BF16> {
 template <> struct RowMath<KV_F32, AUG_F32> {
   static constexpr int QW = 4;
   using q_t = float;
+  using k_t = uint4;
+  __device__ static const uint4& prep(const uint4& k) { return k; }
   __device__ static void load(const void* q, int64_t off, q_t* dst) {
     const float4 v = *reinterpret_cast<const float4*>(static_cast<const float*>(q) + off);
     dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
@@ -207,22 +211,24 @@ template <> struct RowMath<KV_F32, AUG_F32> {
   }
 };
 
+// fp8 K is converted once per load to packed bf16 (exact for OCP E4M3FN)
+// and dotted with the bf16 query pairs like the bf16 cache.
 template <> struct RowMath<KV_FP8, AUG_BF16> {
-  static constexpr int QW = 8;
-  using q_t = float;
+  static constexpr int QW = 4;
+  using q_t = uint32_t;
+  using k_t = uint4;
   __device__ static void load(const void* q, int64_t off, q_t* dst) {
-    const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(q) + off);
-    dst[0] = bf16_lo(v.x); dst[1] = bf16_hi(v.x); dst[2] = bf16_lo(v.y); dst[3] = bf16_hi(v.y);
-    dst[4] = bf16_lo(v.z); dst[5] = bf16_hi(v.z); dst[6] = bf16_lo(v.w); dst[7] = bf16_hi(v.w);
+    RowMath<KV_BF16, AUG_BF16>::load(q, off, dst);
   }
-  __device__ static float dot(const q_t* qh, const uint2& k) {
-    float kf[8];
-    KvFmt<KV_FP8>::to_f32(k, kf);
-    float acc = qh[0] * kf[0];
-#pragma unroll
-    for (int e = 1; e < 8; ++e) acc = fmaf(qh[e], kf[e], acc);
-    return acc;
+  __device__ static uint4 prep(const uint2& k) {
+    uint4 o;
+    o.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(k.x, 1.0f, false));
+    o.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(k.x, 1.0f, true));
+    o.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(k.y, 1.0f, false));
+    o.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(k.y, 1.0f, true));
+    return o;
   }
+  __device__ static float dot(const q_t* qh, const uint4& k) { return RowMath<KV_BF16, AUG_BF16>::dot(qh, k); }
 };
 
 // ---------------------------------------------------------------------------
@@ -274,7 +280,7 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   // The block id of a wave's next block is fetched one iteration ahead, so
   // the K/V loads of a block never wait on the block-table load. With
   // PREFETCH the K/V of the next block are in flight too while the current
-  // one is computed (used where occupancy is low anyway).
+  // one is computed.
   constexpr int kWaves = kThreads / 64;
   const int32_t* table = a.block_ids + it.bt_off + blk0;
   auto load_block = [&](int bid, elem_t* kr, elem_t* vr) {
@@ -339,8 +345,9 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
     float s[NLD][G];
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
+      const typename M::k_t kb = M::prep(kraw[i]);
 #pragma unroll
-      for (int h = 0; h < G; ++h) s[i][h] = group_sum<LPT>(M::dot(q[h], kraw[i])) * ksc;
+      for (int h = 0; h < G; ++h) s[i][h] = group_sum<LPT>(M::dot(q[h], kb)) * ksc;
     }
     if (!full) {
 #pragma unroll
@@ -853,7 +860,9 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
       return;
     }
   }
-  row_item<KVT, D, G, QT, OT, TILES>(it, a, reinterpret_cast<float*>(smem));
+  // row items always fetch a wave's next block while the current one is
+  // computed: short spans (small batches) are latency bound otherwise
+  row_item<KVT, D, G, QT, OT, true>(it, a, reinterpret_cast<float*>(smem));
 }
 
 // Batches without prefill tiles: row items only, sized for high occupancy.

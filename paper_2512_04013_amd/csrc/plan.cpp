@@ -71,14 +71,14 @@ struct Sized {
 // tiles. Calibrated on MI355X: a row item streams its K/V at about 11.5 GB/s
 // per resident workgroup (5.9 TB/s over 512); a tile item costs about 3 us
 // of set-up and write-out plus 2.6 us per 64-key step of its 128 rows; the
-// split-K merge launch about 5 us plus its partials read at 1.5 bytes/ns.
+// split-K merge launch about 5 us plus its partials read at 1.5 TB/s.
 constexpr int kSlots = 512;
 double row_item_ns(int64_t keys, int32_t head_dim, int32_t kv_bytes) {
   return static_cast<double>(keys) * head_dim * kv_bytes * 2 / 11.5;
 }
 double tile_item_ns(int64_t key_tiles) { return 3000.0 + static_cast<double>(key_tiles) * 2600.0; }
 double merge_ns(int64_t partial_bytes) {
-  return partial_bytes > 0 ? 5000.0 + static_cast<double>(partial_bytes) / 1.5 : 0.0;
+  return partial_bytes > 0 ? 5000.0 + static_cast<double>(partial_bytes) / 1500.0 : 0.0;
 }
 
 // Lower bound of a launch's makespan on kSlots slots: its longest item, or
@@ -87,12 +87,13 @@ double makespan_bound(double longest, double total) { return std::max(longest, t
 
 int32_t choose_split(int64_t total_row_keys, int32_t requested) {
   if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;
-  // About four row items per compute unit (256 CUs) on small batches; on
-  // large ones spans of 4096 keys, long enough that an item's fixed costs
-  // (query load, state merge, partial write) are a few percent of its
-  // streaming time while lognormal context mixes still balance.
+  // About four row items per compute unit (256 CUs), but never spans under
+  // 512 keys (on small batches an item's fixed latency, query load, state
+  // merge and partial write, outweighs shorter streams); on large batches
+  // spans of 4096 keys, long enough that those fixed costs are a few percent
+  // of an item's streaming time while lognormal context mixes still balance.
   int64_t s = (total_row_keys + 1023) / 1024;
-  s = std::max<int64_t>(s, 256);
+  s = std::max<int64_t>(s, 512);
   s = std::min<int64_t>(s, 4096);
   return static_cast<int32_t>(((s + kBlock - 1) / kBlock) * kBlock);
 }
@@ -176,7 +177,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
     }
     double best = 0.0;
     bool have = false;
-    for (const int32_t cand : {kTileSpanMax, 4096, 2048, kTileSpanMin}) {
+    for (const int32_t cand : {kTileSpanMax, 4096, 2048, 1024, 512, kTileSpanMin}) {
       if (have && longest_tile <= cand) continue;   // nothing splits: same as the longer span
       double total = row_total, longest = row_longest;
       int64_t partial_bytes = row_partial_bytes;

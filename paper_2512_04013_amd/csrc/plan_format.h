@@ -11,7 +11,7 @@ constexpr int32_t kPlanVersion = 1;
 constexpr int32_t kBlock = 16;              // tokens per KV block
 constexpr int32_t kKeyTile = 64;            // keys per MFMA tile (4 blocks)
 constexpr int32_t kTileRows = 128;          // query rows (positions x group heads) per MFMA tile
-constexpr int32_t kTileSpanMin = 1024;      // a tile is never split into spans shorter than this
+constexpr int32_t kTileSpanMin = 256;       // a tile is never split into spans shorter than this
 constexpr int32_t kTileSpanMax = 8192;      // longest key span of one tile item (its block ids fit in LDS)
 
 enum ItemKind : int32_t {
