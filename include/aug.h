@@ -17,7 +17,7 @@
  *   aug_attn_plan     host: validates a formed batch and writes the work list
  *   aug_attn_mixed    device: one launch of paged, causal, grouped-query
  *                     attention over every chunked-prefill row and decode row
- *                     of the batch (plus a split-K merge launch when needed)
+ *                     of the batch (plus a merge launch for split prefill tiles)
  *   aug_kv_park       device -> pinned host: swap-out of KV blocks
  *   aug_kv_resume     pinned host -> device: swap-in into (new) KV blocks
  *
@@ -114,12 +114,13 @@ typedef struct {
   int64_t workspace_bytes;   /* device workspace aug_attn_mixed needs */
   int32_t num_items;         /* work items of the attention launch */
   int32_t num_prefill_items; /* of which chunked-prefill tiles */
-  int32_t num_merge_groups;  /* (request, KV head) pairs whose keys are split */
+  int32_t num_merge_groups;  /* split (row, KV head) pairs; the first num_tile_merge_groups
+                                belong to prefill tiles */
   int32_t num_partials;      /* split-K partial results */
   int32_t kv_split_tokens;   /* keys per decode work item (multiple of block_size) */
   int32_t total_rows;        /* q_start[num_reqs] */
   int32_t num_reqs;
-  int32_t reserved;
+  int32_t num_tile_merge_groups;
 } aug_attn_plan_info;
 
 /* Validate a formed batch and write its work list ("plan image") to
@@ -139,7 +140,11 @@ aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batc
 /* Mixed-batch paged attention: for every row of every request of the planned
  * batch, O = softmax(softmax_scale * q K^T, causal) V over the request's
  * paged keys (see aug_batch_desc). Device memory:
- *   plan_dev   the plan image of aug_attn_plan (info->plan_bytes bytes)
+ *   plan_dev   the plan image of aug_attn_plan (info->plan_bytes bytes). Its
+ *              last 4 * info->num_merge_groups bytes are completion counters
+ *              of the split decode rows, which the launch increments and
+ *              returns to zero, so the same device copy can be launched
+ *              again; calls that overlap on one copy race
  *   q          [total_rows][num_q_heads][head_dim], q_dtype
  *   k_cache,   [num_pool_blocks][num_kv_heads][block_size][head_dim], kv_dtype
  *   v_cache
@@ -150,13 +155,14 @@ aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batc
  *   workspace  >= info->workspace_bytes bytes (split-K partials); contents on
  *              entry do not matter
  * Slots past a request's context and blocks it does not list never influence
- * its output, whatever they hold. Enqueued on `stream`; one kernel launch,
- * plus a second small launch that merges split-K partials when
- * info->num_merge_groups > 0.
+ * its output, whatever they hold. Enqueued on `stream` as one kernel launch:
+ * split decode rows are merged in it by the workgroup that finishes each
+ * row's last span; split prefill tiles are merged by a second small launch
+ * when info->num_tile_merge_groups > 0.
  * Errors: AUG_ERR_INVALID (NULL pointers, info/shape mismatch),
  * AUG_ERR_NO_SPACE (workspace_bytes too small), AUG_ERR_HIP (launch). */
 aug_status aug_attn_mixed(const aug_attn_shape* shape, const aug_attn_plan_info* info,
-                          const void* plan_dev, const void* q, const void* k_cache,
+                          void* plan_dev, const void* q, const void* k_cache,
                           const void* v_cache, const float* k_scale, const float* v_scale,
                           const int32_t* block_ids, int32_t num_pool_blocks, void* out,
                           void* workspace, size_t workspace_bytes, void* stream);

@@ -59,7 +59,8 @@ class aug_attn_plan_info(C.Structure):
     _fields_ = [("plan_bytes", C.c_int64), ("workspace_bytes", C.c_int64), ("num_items", C.c_int32),
                 ("num_prefill_items", C.c_int32), ("num_merge_groups", C.c_int32),
                 ("num_partials", C.c_int32), ("kv_split_tokens", C.c_int32),
-                ("total_rows", C.c_int32), ("num_reqs", C.c_int32), ("reserved", C.c_int32)]
+                ("total_rows", C.c_int32), ("num_reqs", C.c_int32),
+                ("num_tile_merge_groups", C.c_int32)]
 
 
 class aug_request(C.Structure):

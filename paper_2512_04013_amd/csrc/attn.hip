@@ -29,9 +29,13 @@
 // and their scores masked, so NaN or garbage in unused slots cannot leak.
 // Block ids outside the pool are treated the same way (never dereferenced).
 //
-// Split-K: a row item whose request was split writes an unnormalised partial
-// (o, m, l) to the workspace; a second, small launch merges the partials of
-// each (row, KV head) by log-sum-exp.
+// Split-K: an item whose keys were split writes an unnormalised partial
+// (o, m, l) per row to the workspace. A decode row's span then counts itself
+// done on its group's counter in the plan image, and the workgroup that
+// finishes the row's last span merges its partials by log-sum-exp (and
+// resets the counter) in the same launch. Split prefill tiles, whose rows
+// would make one workgroup merge many rows serially, are merged by a second
+// launch, one workgroup per (row, KV head).
 
 #include <hip/hip_runtime.h>
 
@@ -77,6 +81,8 @@ struct AttnArgs {
   const int32_t* block_ids;
   void* out;
   float* partials;
+  const MergeGroup* groups;   // split groups of the plan
+  int32_t* counters;          // per group: spans finished in this launch (zero between launches)
   int32_t num_pool_blocks;
   int32_t hq;
   int32_t hkv;
@@ -230,6 +236,122 @@ template <> struct RowMath<KV_FP8, AUG_BF16> {
   }
   __device__ static float dot(const q_t* qh, const uint4& k) { return RowMath<KV_BF16, AUG_BF16>::dot(qh, k); }
 };
+
+// ---------------------------------------------------------------------------
+// split-K merge inside the launch
+// ---------------------------------------------------------------------------
+
+// Partials cross workgroups that may run on different XCDs, whose L2 caches
+// are not coherent with each other. They are therefore stored and loaded as
+// device-scope relaxed atomics (write-through / coherent accesses), and a
+// writer waits for its stores to complete before it counts its span done;
+// no release fence, which would write back and invalidate the whole L2.
+__device__ __forceinline__ void store_partial(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_partial(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Merge the partials of one (row, KV head) group with a workgroup of NT
+// threads: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s.
+// The (m, l) pairs are staged in LDS (kMergeStage x 2G floats) so the output
+// loads of all partials are independent; the per-head running maximum, sum
+// and rescale factor follow them in LDS (3G floats), kept by threads 0..G-1.
+constexpr int kMergeStage = 64;   // partials staged per pass
+constexpr int merge_lds_floats(int g) { return kMergeStage * 2 * g + 3 * g; }
+
+template <int D, int G, int OT, int NT>
+__device__ __forceinline__ void merge_group(const MergeGroup& g, const float* partials, void* out, int32_t hq,
+                                            float* lds) {
+  static_assert(G <= NT, "one thread per head keeps the running statistics");
+  const int64_t pf = aug::partial_floats(G, D);
+  constexpr int PER = (G * D + NT - 1) / NT;   // output elements per thread
+  float* ml = lds;
+  float* run_m = lds + kMergeStage * 2 * G;
+  float* run_l = run_m + G;
+  float* rescale = run_l + G;
+  float acc[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) acc[k] = 0.f;
+  if (threadIdx.x < G) {
+    run_m[threadIdx.x] = kNegBig;
+    run_l[threadIdx.x] = 0.f;
+  }
+  for (int s0 = 0; s0 < g.n_parts; s0 += kMergeStage) {
+    const int ns = min(kMergeStage, g.n_parts - s0);
+    __syncthreads();
+    for (int i = threadIdx.x; i < ns * 2 * G; i += NT) {
+      const int s = i / (2 * G);
+      const int j = i % (2 * G);
+      ml[s * 2 * G + j] = load_partial(partials + (g.part0 + s0 + s) * pf + G * D + j);
+    }
+    __syncthreads();
+    if (threadIdx.x < G) {
+      // this pass's maximum for head h, and the rescaling of what earlier passes summed
+      const int h = threadIdx.x;
+      float m = run_m[h];
+      for (int s = 0; s < ns; ++s) m = fmaxf(m, ml[s * 2 * G + h]);
+      const float old = __builtin_amdgcn_exp2f(run_m[h] - m);
+      float l = run_l[h] * old;
+      for (int s = 0; s < ns; ++s) l += ml[s * 2 * G + G + h] * __builtin_amdgcn_exp2f(ml[s * 2 * G + h] - m);
+      run_m[h] = m;
+      run_l[h] = l;
+      rescale[h] = old;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int idx = threadIdx.x + k * NT;
+      if (idx >= G * D) break;
+      const int h = idx / D;
+      const float mh = run_m[h];
+      float o = acc[k] * rescale[h];
+      const float* base = partials + static_cast<int64_t>(g.part0 + s0) * pf + idx;
+      int s = 0;
+      for (; s + 4 <= ns; s += 4) {
+        const float o0 = load_partial(base + (s + 0) * pf), o1 = load_partial(base + (s + 1) * pf);
+        const float o2 = load_partial(base + (s + 2) * pf), o3 = load_partial(base + (s + 3) * pf);
+        o += o0 * __builtin_amdgcn_exp2f(ml[(s + 0) * 2 * G + h] - mh);
+        o += o1 * __builtin_amdgcn_exp2f(ml[(s + 1) * 2 * G + h] - mh);
+        o += o2 * __builtin_amdgcn_exp2f(ml[(s + 2) * 2 * G + h] - mh);
+        o += o3 * __builtin_amdgcn_exp2f(ml[(s + 3) * 2 * G + h] - mh);
+      }
+      for (; s < ns; ++s) o += load_partial(base + s * pf) * __builtin_amdgcn_exp2f(ml[s * 2 * G + h] - mh);
+      acc[k] = o;
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int idx = threadIdx.x + k * NT;
+    if (idx >= G * D) break;
+    const int h = idx / D;
+    const int d = idx % D;
+    const int64_t off = (static_cast<int64_t>(g.q_row) * hq + static_cast<int64_t>(g.kvh) * G + h) * D + d;
+    store_out<OT>(out, off, acc[k] / run_l[h]);
+  }
+}
+
+// Called by every thread of a split item after it stored its partials. The
+// workgroup that finishes a group's last span merges the group's rows
+// (merge groups `group` .. `group + n_rows - 1`, which share their spans) and
+// returns the counter to zero, so the plan image can be launched again.
+// `lds` needs merge_lds_floats(G) + 1 floats and must be free when this is called.
+template <int D, int G, int OT, int NT>
+__device__ __forceinline__ void finish_split(const AttnArgs& a, int group, int n_rows, float* lds) {
+  __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores have completed
+  __syncthreads();
+  int* flag = reinterpret_cast<int*>(lds + merge_lds_floats(G));
+  if (threadIdx.x == 0) {
+    const int done = __hip_atomic_fetch_add(a.counters + group, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = done == a.groups[group].n_parts - 1;
+    if (last) __hip_atomic_store(a.counters + group, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = last;
+  }
+  __syncthreads();
+  if (!*flag) return;
+  for (int r = 0; r < n_rows; ++r) merge_group<D, G, OT, NT>(a.groups[group + r], a.partials, a.out, a.hq, lds);
+}
 
 // ---------------------------------------------------------------------------
 // row items (VALU)
@@ -450,13 +572,14 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
       store_out<OT>(a.out, off, os / ls);
     } else {
       float* pp = a.partials + static_cast<int64_t>(it.part) * aug::partial_floats(G, D);
-      pp[h * D + d] = os;
+      store_partial(pp + h * D + d, os);
       if (d == 0) {
-        pp[G * D + h] = mx;
-        pp[G * D + G + h] = ls;
+        store_partial(pp + G * D + h, mx);
+        store_partial(pp + G * D + G + h, ls);
       }
     }
   }
+  if (it.part >= 0) finish_split<D, G, OT, kThreads>(a, it.group, 1, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -803,8 +926,8 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   for (; t < t1; ++t) step(t, bool_tag<true>{});
 
   const float l_tot = sum_across_halves(l_run);
-  if (!row_ok) return;
   if (it.part < 0) {
+    if (!row_ok) return;
     const float inv = 1.f / l_tot;
     const int64_t ooff = (static_cast<int64_t>(it.q_row0 + p) * a.hq + static_cast<int64_t>(kvh) * G + gh) * D;
 #pragma unroll
@@ -824,7 +947,9 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
         }
       }
   } else {
-    // split tile: unnormalised partial of this row for head gh
+    // split tile: unnormalised partial of this row for head gh, merged by
+    // the tile merge launch after this one
+    if (!row_ok) return;
     float* pp = a.partials + static_cast<int64_t>(it.part + p * it.part_stride) * aug::partial_floats(G, D);
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -852,6 +977,8 @@ template <int KVT, int D, int G, int QT, int OT, bool TILES>
 __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   constexpr int RB = row_lds_bytes<D, G>();
   constexpr int TB = TILES ? TileLds<D>::BYTES : 0;
+  static_assert(RB >= (merge_lds_floats(G) + 1) * 4 && (!TILES || TB >= (merge_lds_floats(G) + 1) * 4),
+                "a split item's workgroup merges in its own LDS");
   __shared__ __align__(16) unsigned char smem[RB > TB ? RB : TB];
   const WorkItem it = a.items[blockIdx.x];
   if constexpr (TILES) {
@@ -879,83 +1006,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   attn_body<KVT, D, G, QT, OT, true>(a);
 }
 
-// Merge the split-K partials of each (row, KV head): O = sum_s o_s 2^(m_s-M) /
-// sum_s l_s 2^(m_s-M), M = max_s m_s. The (m, l) pairs of all partials are
-// staged in LDS first so the output loads of every partial are independent.
-constexpr int kMaxMergeStage = 64;   // partials staged per pass
-
+// Merge launch for split prefill tiles: one workgroup per (row, KV head)
+// group; the attention launch before it wrote the partials.
 template <int D, int G, int OT>
-__global__ __launch_bounds__(kThreads) void merge_kernel(const MergeGroup* groups, const float* partials,
-                                                         void* out, int32_t hq) {
-  __shared__ float ml[kMaxMergeStage][2 * G];
-  const MergeGroup g = groups[blockIdx.x];
-  const int64_t pf = aug::partial_floats(G, D);
-  constexpr int PER = (G * D + kThreads - 1) / kThreads;   // output elements per thread
-  float acc[PER];
-#pragma unroll
-  for (int k = 0; k < PER; ++k) acc[k] = 0.f;
-  float run_m[G], run_l[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    run_m[h] = kNegBig;
-    run_l[h] = 0.f;
-  }
-  for (int s0 = 0; s0 < g.n_parts; s0 += kMaxMergeStage) {
-    const int ns = min(kMaxMergeStage, g.n_parts - s0);
-    __syncthreads();
-    for (int i = threadIdx.x; i < ns * 2 * G; i += kThreads) {
-      const int s = i / (2 * G);
-      const int j = i % (2 * G);
-      ml[s][j] = partials[(g.part0 + s0 + s) * pf + G * D + j];
-    }
-    __syncthreads();
-    // per head: the pass maximum, rescaling of what earlier passes summed
-    float pm[G], scale_old[G];
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float m = run_m[h];
-      for (int s = 0; s < ns; ++s) m = fmaxf(m, ml[s][h]);
-      scale_old[h] = __builtin_amdgcn_exp2f(run_m[h] - m);
-      pm[h] = m;
-      float l = run_l[h] * scale_old[h];
-      for (int s = 0; s < ns; ++s) l += ml[s][G + h] * __builtin_amdgcn_exp2f(ml[s][h] - m);
-      run_l[h] = l;
-      run_m[h] = m;
-    }
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int idx = threadIdx.x + k * kThreads;
-      if (idx >= G * D) break;
-      const int h = idx / D;
-      float o = acc[k] * scale_old[h];
-      const float* base = partials + static_cast<int64_t>(g.part0 + s0) * pf + idx;
-      int s = 0;
-      for (; s + 4 <= ns; s += 4) {
-        const float o0 = base[(s + 0) * pf], o1 = base[(s + 1) * pf];
-        const float o2 = base[(s + 2) * pf], o3 = base[(s + 3) * pf];
-        o += o0 * __builtin_amdgcn_exp2f(ml[s + 0][h] - pm[h]);
-        o += o1 * __builtin_amdgcn_exp2f(ml[s + 1][h] - pm[h]);
-        o += o2 * __builtin_amdgcn_exp2f(ml[s + 2][h] - pm[h]);
-        o += o3 * __builtin_amdgcn_exp2f(ml[s + 3][h] - pm[h]);
-      }
-      for (; s < ns; ++s) o += base[s * pf] * __builtin_amdgcn_exp2f(ml[s][h] - pm[h]);
-      acc[k] = o;
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int idx = threadIdx.x + k * kThreads;
-    if (idx >= G * D) break;
-    const int h = idx / D;
-    const int d = idx % D;
-    const int64_t off = (static_cast<int64_t>(g.q_row) * hq + static_cast<int64_t>(g.kvh) * G + h) * D + d;
-    store_out<OT>(out, off, acc[k] / run_l[h]);
-  }
+__global__ __launch_bounds__(kThreads) void tile_merge_kernel(AttnArgs a) {
+  __shared__ float lds[merge_lds_floats(G)];
+  merge_group<D, G, OT, kThreads>(a.groups[blockIdx.x], a.partials, a.out, a.hq, lds);
 }
 
 template <int KVT, int D, int G, int QT, int OT>
-aug_status launch(const AttnArgs& a, const aug_attn_plan_info& info, const MergeGroup* groups,
-                  hipStream_t st) {
+aug_status launch(const AttnArgs& a, const aug_attn_plan_info& info, hipStream_t st) {
   if (info.num_items > 0) {
     if (info.num_prefill_items > 0) {
       if constexpr ((KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16) {
@@ -969,9 +1029,8 @@ aug_status launch(const AttnArgs& a, const aug_attn_plan_info& info, const Merge
     if (hipError_t e = hipGetLastError(); e != hipSuccess)
       return aug::fail(AUG_ERR_HIP, "aug_attn_mixed: launch failed: %s", hipGetErrorString(e));
   }
-  if (info.num_merge_groups > 0) {
-    hipLaunchKernelGGL((merge_kernel<D, G, OT>), dim3(info.num_merge_groups), dim3(kThreads), 0, st,
-                       groups, a.partials, a.out, a.hq);
+  if (info.num_tile_merge_groups > 0) {
+    hipLaunchKernelGGL((tile_merge_kernel<D, G, OT>), dim3(info.num_tile_merge_groups), dim3(kThreads), 0, st, a);
     if (hipError_t e = hipGetLastError(); e != hipSuccess)
       return aug::fail(AUG_ERR_HIP, "aug_attn_mixed: merge launch failed: %s", hipGetErrorString(e));
   }
@@ -980,9 +1039,9 @@ aug_status launch(const AttnArgs& a, const aug_attn_plan_info& info, const Merge
 
 template <int KVT, int QT, int OT>
 aug_status dispatch_dg(int d, int g, const AttnArgs& a, const aug_attn_plan_info& info,
-                       const MergeGroup* groups, hipStream_t st) {
+                       hipStream_t st) {
 #define AUG_CASE(DD, GG) \
-  if (d == DD && g == GG) return launch<KVT, DD, GG, QT, OT>(a, info, groups, st);
+  if (d == DD && g == GG) return launch<KVT, DD, GG, QT, OT>(a, info, st);
   if constexpr (KVT != KV_FP8) {
     AUG_CASE(64, 1) AUG_CASE(64, 2) AUG_CASE(64, 4) AUG_CASE(64, 8)
   }
@@ -994,7 +1053,7 @@ aug_status dispatch_dg(int d, int g, const AttnArgs& a, const aug_attn_plan_info
 }  // namespace
 
 extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_plan_info* info,
-                                     const void* plan_dev, const void* q, const void* k_cache,
+                                     void* plan_dev, const void* q, const void* k_cache,
                                      const void* v_cache, const float* k_scale, const float* v_scale,
                                      const int32_t* block_ids, int32_t num_pool_blocks, void* out,
                                      void* workspace, size_t workspace_bytes, void* stream) {
@@ -1002,9 +1061,10 @@ extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_pla
   if (aug_status st = aug::check_shape(s, who); st != AUG_OK) return st;
   if (!info) return aug::fail(AUG_ERR_INVALID, "%s: info is NULL", who);
   if (info->num_items < 0 || info->num_merge_groups < 0 || info->num_partials < 0 ||
+      info->num_tile_merge_groups < 0 || info->num_tile_merge_groups > info->num_merge_groups ||
       info->plan_bytes != static_cast<int64_t>(sizeof(aug::PlanHeader)) +
                               static_cast<int64_t>(info->num_items) * sizeof(WorkItem) +
-                              static_cast<int64_t>(info->num_merge_groups) * sizeof(MergeGroup))
+                              static_cast<int64_t>(info->num_merge_groups) * (sizeof(MergeGroup) + 4))
     return aug::fail(AUG_ERR_INVALID, "%s: info is inconsistent", who);
   if (info->num_items == 0) return AUG_OK;
   if (!plan_dev || !q || !k_cache || !v_cache || !block_ids || !out)
@@ -1017,10 +1077,12 @@ extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_pla
                      (long long)info->workspace_bytes);
 
   AttnArgs a{};
-  const auto* base = static_cast<const unsigned char*>(plan_dev);
+  auto* base = static_cast<unsigned char*>(plan_dev);
+  const size_t groups_off = sizeof(aug::PlanHeader) + static_cast<size_t>(info->num_items) * sizeof(WorkItem);
   a.items = reinterpret_cast<const WorkItem*>(base + sizeof(aug::PlanHeader));
-  const auto* groups = reinterpret_cast<const MergeGroup*>(
-      base + sizeof(aug::PlanHeader) + static_cast<size_t>(info->num_items) * sizeof(WorkItem));
+  a.groups = reinterpret_cast<const MergeGroup*>(base + groups_off);
+  a.counters = reinterpret_cast<int32_t*>(base + groups_off +
+                                          static_cast<size_t>(info->num_merge_groups) * sizeof(MergeGroup));
   a.q = q;
   a.k_cache = k_cache;
   a.v_cache = v_cache;
@@ -1035,7 +1097,7 @@ extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_pla
   a.scale_log2 = s->softmax_scale * kLog2e;
   const int g = s->num_q_heads / s->num_kv_heads;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (s->kv_dtype == AUG_F32) return dispatch_dg<KV_F32, AUG_F32, AUG_F32>(s->head_dim, g, a, *info, groups, st);
-  if (s->kv_dtype == AUG_BF16) return dispatch_dg<KV_BF16, AUG_BF16, AUG_BF16>(s->head_dim, g, a, *info, groups, st);
-  return dispatch_dg<KV_FP8, AUG_BF16, AUG_BF16>(s->head_dim, g, a, *info, groups, st);
+  if (s->kv_dtype == AUG_F32) return dispatch_dg<KV_F32, AUG_F32, AUG_F32>(s->head_dim, g, a, *info, st);
+  if (s->kv_dtype == AUG_BF16) return dispatch_dg<KV_BF16, AUG_BF16, AUG_BF16>(s->head_dim, g, a, *info, st);
+  return dispatch_dg<KV_FP8, AUG_BF16, AUG_BF16>(s->head_dim, g, a, *info, st);
 }

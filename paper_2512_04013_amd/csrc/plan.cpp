@@ -13,6 +13,7 @@
 // is deterministic and validates the batch completely before any launch.
 
 #include <algorithm>
+#include <cstdint>
 #include <cmath>
 #include <cstring>
 #include <vector>
@@ -235,6 +236,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
                       "tile spans are whole key tiles");
         // span <= tile_span <= kTileSpanMax, so the kernel's per-item block-id buffer suffices
         for (int32_t h = 0; h < hkv; ++h) {
+          const int32_t g0 = static_cast<int32_t>(tile_groups.size());
           for (int32_t sidx = 0; sidx < nsp; ++sidx) {
             WorkItem it{};
             it.kvh = static_cast<int16_t>(h);
@@ -247,6 +249,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
             it.pos0 = pos0;
             it.bt_off = b->bt_start[r];
             it.part = nsp > 1 ? static_cast<int32_t>(tile_parts) + sidx : -1;
+            it.group = nsp > 1 ? g0 : -1;
             const int64_t steps = (it.key_end - it.key_begin + kKeyTile - 1) / kKeyTile;
             tiles.push_back({it, tile_item_ns(steps), order++});
           }
@@ -293,7 +296,10 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   const int64_t n_parts = tile_parts + row_parts;
   if (n_parts > (int64_t{1} << 30))
     return fail(AUG_ERR_UNSUPPORTED, "%s: %lld split-K partials", who, (long long)n_parts);
-  const int64_t plan_bytes = groups_off + n_groups * static_cast<int64_t>(sizeof(MergeGroup));
+  const int64_t counters_off = groups_off + n_groups * static_cast<int64_t>(sizeof(MergeGroup));
+  const int64_t plan_bytes = counters_off + n_groups * 4;
+  if (plan_bytes > INT32_MAX)
+    return fail(AUG_ERR_UNSUPPORTED, "%s: plan image of %lld bytes", who, (long long)plan_bytes);
   const int64_t ws = ((n_parts * partial_floats(g, s->head_dim) * 4 + 255) / 256) * 256;
 
   std::memset(info, 0, sizeof(*info));
@@ -306,6 +312,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   info->kv_split_tokens = split;
   info->total_rows = static_cast<int32_t>(total_rows);
   info->num_reqs = n;
+  info->num_tile_merge_groups = static_cast<int32_t>(tile_groups.size());
   if (!plan_host) return AUG_OK;
   if (plan_cap < static_cast<size_t>(plan_bytes))
     return fail(AUG_ERR_NO_SPACE, "%s: plan buffer %zu < %lld bytes", who, plan_cap,
@@ -323,6 +330,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   hdr.total_rows = info->total_rows;
   hdr.items_offset = static_cast<int32_t>(items_off);
   hdr.groups_offset = static_cast<int32_t>(groups_off);
+  hdr.counters_offset = static_cast<int32_t>(counters_off);
   std::memcpy(base, &hdr, sizeof(hdr));
   auto* items = reinterpret_cast<WorkItem*>(base + items_off);
   auto* groups = reinterpret_cast<MergeGroup*>(base + groups_off);
@@ -345,6 +353,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
       const int32_t nspan = (keys + rr.span - 1) / rr.span;
       for (int32_t h = 0; h < hkv; ++h) {
         const int32_t part0 = nspan > 1 ? parts : -1;
+        const int32_t group = nspan > 1 ? ng : -1;
         if (nspan > 1) {
           groups[ng++] = MergeGroup{b->q_start[r] + j, h, part0, nspan};
           parts += nspan;
@@ -361,11 +370,13 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
           it.pos0 = pos;
           it.bt_off = b->bt_start[r];
           it.part = nspan > 1 ? part0 + sidx : -1;
+          it.group = group;
           items[k++] = it;
         }
       }
     }
   }
   emit_tiles_longer_than(-1.0);
+  std::memset(base + counters_off, 0, static_cast<size_t>(n_groups) * 4);
   return AUG_OK;
 }

@@ -30,13 +30,14 @@ struct PlanHeader {          // 64 bytes
   int32_t total_rows;
   int32_t items_offset;      // bytes from the start of the image
   int32_t groups_offset;
-  int32_t reserved[6];
+  int32_t counters_offset;   // int32 per merge group, zero in the image
+  int32_t reserved[5];
 };
 
-struct WorkItem {            // 32 bytes
+struct WorkItem {            // 48 bytes
   int16_t kvh;               // KV head
   int8_t kind;               // ItemKind
-  int8_t reserved;
+  int8_t reserved0;
   int32_t q_row0;            // first global row of Q/O
   int16_t n_rows;            // rows (context positions) in the item
   int16_t part_stride;       // tiles: distance between the partial slots of consecutive rows
@@ -45,6 +46,12 @@ struct WorkItem {            // 32 bytes
   int32_t pos0;              // context position of the first row
   int32_t bt_off;            // offset of the request's block table in block_ids
   int32_t part;              // partial slot of the first row, -1 = write O directly
+  // split items: merge group of the first row (the item's rows own groups
+  // group .. group + n_rows - 1, which share their spans); that group's
+  // counter counts finished spans and its n_parts is the number of spans.
+  // -1 when not split.
+  int32_t group;
+  int32_t reserved[3];
 };
 
 struct MergeGroup {          // 16 bytes
@@ -55,7 +62,7 @@ struct MergeGroup {          // 16 bytes
 };
 
 static_assert(sizeof(PlanHeader) == 64, "plan header layout");
-static_assert(sizeof(WorkItem) == 32, "work item layout");
+static_assert(sizeof(WorkItem) == 48, "work item layout");
 static_assert(sizeof(MergeGroup) == 16, "merge group layout");
 
 // Split-K partial of one (row, KV head, key span): unnormalised o[G][D]

@@ -73,6 +73,32 @@ def test_ragged_shapes(case, sharp):
         compare(got, want, qd, what=f"case{case} sharp={sharp} split={split} tiles={att.info.num_prefill_items}")
 
 
+def test_relaunching_one_plan_image_repeats_the_bits():
+    """Split decode rows are merged inside the launch through completion
+    counters in the plan image, which the launch returns to zero: the same
+    device copy launched again gives the same bits, and the counters read
+    zero afterwards."""
+    q_lens, ctx_lens, hq, hkv, d, dt = CASES[9]
+    b = make_batch_from_lengths("relaunch", q_lens, ctx_lens, num_q_heads=hq, num_kv_heads=hkv,
+                                head_dim=d, q_dtype="bf16", kv_dtype=dt, out_dtype="bf16",
+                                n_pool_blocks=512, seed=77, kv_std=1.0 / np.sqrt(d))
+    say("[relaunch] fp8 G=8, split rows and tiles, 4 launches of one plan image")
+    first, att = _run(b, kv_split=32)
+    assert att.info.num_merge_groups > att.info.num_tile_merge_groups > 0
+    compare(first, oa.attention_for(b), "bf16", what="relaunch first")
+    from paper_2512_04013_amd import runtime as rt
+    q = rt.to_device_array(b.q, b.q_dtype, "cuda")
+    for i in range(3):
+        att.out.zero_()
+        got = rt.to_host_f64(att.run(q))
+        torch.cuda.synchronize()
+        assert np.array_equal(got.view(np.uint64), first.view(np.uint64)), f"launch {i + 2} differs"
+    image = att.plan_dev.cpu().numpy()
+    hdr = image[:64].view(np.int32)
+    counters = image[hdr[10]:hdr[10] + 4 * att.info.num_merge_groups].view(np.int32)
+    assert not counters.any()
+
+
 # ---- the 8B-shaped decode batch at full size ----------------------------------------------------
 
 @pytest.fixture(scope="module")

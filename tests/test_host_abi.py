@@ -40,9 +40,14 @@ def _decode_plan(plan):
     n_items, n_groups = hdr[2], hdr[4]
     item_t = np.dtype([("kvh", "<i2"), ("kind", "i1"), ("res", "i1"), ("q_row0", "<i4"),
                        ("n_rows", "<i2"), ("stride", "<i2"), ("kb", "<i4"), ("ke", "<i4"),
-                       ("pos0", "<i4"), ("bt_off", "<i4"), ("part", "<i4")])
-    items = plan[hdr[8]:hdr[8] + 32 * n_items].view(item_t)
+                       ("pos0", "<i4"), ("bt_off", "<i4"), ("part", "<i4"), ("group", "<i4"),
+                       ("res2", "<i4", (3,))])
+    assert item_t.itemsize == 48
+    items = plan[hdr[8]:hdr[8] + 48 * n_items].view(item_t)
     groups = plan[hdr[9]:hdr[9] + 16 * n_groups].view(np.int32).reshape(-1, 4)
+    counters = plan[hdr[10]:hdr[10] + 4 * n_groups].view(np.int32)
+    assert hdr[10] == hdr[9] + 16 * n_groups and hdr[10] + 4 * n_groups == len(plan)
+    assert not counters.any(), "completion counters start at zero"
     return hdr, items, groups
 
 
@@ -82,6 +87,11 @@ def test_plan_covers_every_key_of_every_row_once(cfg, split):
                     slot = part + j * stride
                     assert slot not in tile_slots
                     tile_slots.add(slot)
+                    # row j's merge group lists this slot among its spans
+                    q_row, g_kvh, part0, n = groups[int(it["group"]) + j]
+                    assert q_row == row and g_kvh == kvh and part0 <= slot < part0 + n
+            if part < 0:
+                assert int(it["group"]) == -1
         else:
             assert n_rows == 1 and kb % 16 == 0
             pos = b.ctx_len[r] - q_len + (q_row0 - b.q_start[r])
@@ -90,6 +100,10 @@ def test_plan_covers_every_key_of_every_row_once(cfg, split):
             if part >= 0:
                 assert part not in parts_seen
                 parts_seen.add(part)
+                q_row, g_kvh, part0, n = groups[int(it["group"])]
+                assert q_row == q_row0 and g_kvh == kvh and part0 <= part < part0 + n
+            else:
+                assert int(it["group"]) == -1
     assert not (tile_slots & parts_seen)
     parts_seen |= tile_slots
     for r in range(b.num_reqs):
