@@ -149,7 +149,7 @@ def budget_sweep(args, log):
     """Token-budget sweep: for each budget, serve the 2000-request trace with
     the library's former, then replay a sample of the batches it formed (up
     to --sweep-batches, evenly spaced over the run, plus its largest and most
-    prefill-heavy batch) through planner, upload and attention on one 16,384-
+    prefill-heavy batch) through planner, upload and attention on one 65,536-
     block fp8 pool of random codes and scales. Reports per budget and overall:
     query tokens per second of the attention launches (HIP events) and of
     whole replayed steps, and the fractions of the HBM and MFMA roofs."""
@@ -172,7 +172,9 @@ def budget_sweep(args, log):
         log(f"budget {budget}: {n} batches formed ({'whole trace' if run.complete else 'overloaded, stopped'}), "
             f"{len(pick)} replayed ({time.time() - t0:.1f} s)")
     hq, hkv, d = sweep.HEADS_Q, sweep.HEADS_KV, sweep.HEAD_DIM
-    nb = sweep.POOL_BLOCKS
+    # the device pool is four times the simulator's, so the random blocks of
+    # consecutive batches rarely meet in the 256 MB last-level cache
+    nb = 4 * sweep.POOL_BLOCKS
     gen = torch.Generator(device=dev).manual_seed(args.seed)
     shape_kv = (nb, hkv, 16, d)
     sign = torch.randint(0, 2, shape_kv, device=dev, dtype=torch.uint8, generator=gen) << 7
@@ -182,6 +184,7 @@ def budget_sweep(args, log):
     del sign
     k_scale = torch.rand((nb, hkv), device=dev, generator=gen) * 1e-3 + 1e-4
     v_scale = torch.rand((nb, hkv), device=dev, generator=gen) * 1e-3 + 1e-4
+    pool_perm = rng.permutation(nb).astype(np.int32)
     max_rows = max(sum(r.steps[i].q_len) for r, pick in runs.values() for i in pick)
     q = torch.randn((max_rows, hq, d), device=dev, generator=gen).to(torch.bfloat16)
     out = torch.empty((max_rows, hq, d), device=dev, dtype=torch.bfloat16)
@@ -211,7 +214,9 @@ def budget_sweep(args, log):
             q_start[1:] = np.cumsum(q_len)
             bt_start = np.zeros(len(q_len) + 1, np.int32)
             bt_start[1:] = np.cumsum(nblk)
-            bids = rng.permutation(nb)[:int(bt_start[-1])].astype(np.int32)
+            # a random window of one fixed random permutation of the pool
+            # (distinct blocks, O(batch) host work per step)
+            bids = np.take(pool_perm, rng.integers(nb) + np.arange(int(bt_start[-1])), mode="wrap")
             info, plan = aug.aug_attn_plan(shape, q_start, ctx, bt_start, nb, None)
             slot = k & 1
             if host_ev[slot] is not None:
@@ -283,6 +288,9 @@ def main():
     ap.add_argument("--workload", default="decode-8b", choices=sorted(WORKLOADS))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--kv-split", type=int, default=0, help="keys per decode work item (0: planner's choice)")
+    ap.add_argument("--pool-copies", type=int, default=0,
+                    help="copies of the KV pool used in turn (0: enough for 1 GiB of KV reads between "
+                         "two uses of one copy, at most 8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--sweep-batches", type=int, default=200,
@@ -315,7 +323,15 @@ def main():
     log(f"workload {b.name}: {b.num_reqs} requests, {b.total_q} query rows, "
         f"{int(b.ctx_len.sum())} context tokens ({time.time() - t0:.1f} s to generate)")
     shape, kv, q, bids = rt.upload_batch(b, device=dev)
+    # identical copies of the pool, used in turn, so that consecutive steps
+    # never find a small batch's KV in the 256 MB last-level cache
+    touched = algorithmic_bytes(b)
+    n_copies = args.pool_copies or int(min(8, max(1, np.ceil((1 << 30) / touched))))
+    pools = [(kv.k_cache, kv.v_cache, kv.k_scale, kv.v_scale)]
+    for _ in range(n_copies - 1):
+        pools.append(tuple(None if x is None else x.clone() for x in pools[0]))
     torch.cuda.synchronize()
+    log(f"{n_copies} copies of the pool, used in turn")
 
     recs = request_records(b, aug)
     used_blocks = int(np.sum((b.ctx_len.astype(np.int64) + 15) // 16))
@@ -355,7 +371,8 @@ def main():
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        aug.aug_attn_mixed(shape, info, plan_dev, q, kv.k_cache, kv.v_cache, kv.k_scale, kv.v_scale,
+        kc, vc, ksc, vsc = pools[i % len(pools)]
+        aug.aug_attn_mixed(shape, info, plan_dev, q, kc, vc, ksc, vsc,
                            bids, kv.num_pool_blocks, out, ws_dev, stream=stream.cuda_stream)
         e1.record(stream)
         if timed:
@@ -384,7 +401,8 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = 1e3 * elapsed / args.steps
-    attn_ms = float(np.mean([a.elapsed_time(c) for a, c in ev]))
+    launch_ms = np.array([a.elapsed_time(c) for a, c in ev])
+    attn_ms = float(launch_ms.mean())
     rows = b.total_q
     value = rows / (elapsed / args.steps)
 
@@ -404,7 +422,9 @@ def main():
             roof["prefill_mfma_tflops"] = round(achieved_tfs, 2)
     roof.update({"kernel": "aug_attn_mixed launches (attention + split-K merge)",
                  "algorithmic_bytes_per_launch": int(nbytes), "prefill_flops_per_launch": int(flops),
-                 "launch_ms": round(attn_ms, 4)})
+                 "launch_ms": round(attn_ms, 4), "launch_ms_median": round(float(np.median(launch_ms)), 4),
+                 "launch_ms_p10": round(float(np.percentile(launch_ms, 10)), 4),
+                 "launch_ms_p90": round(float(np.percentile(launch_ms, 90)), 4)})
 
     result = {
         "metric": "mixed-batch attn query-tokens/s + % peak HBM GB/s (decode) / % MFMA (prefill)",
@@ -415,7 +435,7 @@ def main():
         "config": {"workload": b.name, "requests": b.num_reqs, "query_rows": rows,
                    "context_tokens": int(b.ctx_len.sum()), "q_heads": b.num_q_heads,
                    "kv_heads": b.num_kv_heads, "head_dim": b.head_dim, "block_size": 16,
-                   "kv_split_tokens": int(info.kv_split_tokens), "seed": args.seed},
+                   "kv_split_tokens": int(info.kv_split_tokens), "seed": args.seed, "pool_copies": n_copies},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
