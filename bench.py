@@ -2,9 +2,12 @@
 
 A step is one pass of the hot path over one batch: the host batch former
 (token budget, cost, priority, greedy packing), the host planner, the
-upload of the work list, and the attention launch(es) over the paged cache;
-for workloads that move paused requests it also resumes and parks them.
+upload of the work list, and the attention launch(es) over the paged cache.
 Inputs are synthetic, seeded, and resident in HBM before timing starts.
+Workloads that move paused requests (mixed-8b, long-context-8b) also time
+their resume and park on their own, after the steps, and report them in
+``park_resume`` as GB/s of the host link beside a plain pinned-memory copy of
+the same size; those host transfers are not part of ``value``.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode-8b]
 
@@ -126,6 +129,57 @@ def cpu_baseline(b, budget_s: float = 15.0):
             "kind": "oracle",
             "sample": f"first {n_done} of {b.num_reqs} requests ({done_rows} query rows), float64 numpy, "
                       f"{t_used:.1f} s"}
+
+
+PCIE_PEAK_GBS = 64.0   # PCIe Gen5 x16, per direction
+
+
+def park_resume_rates(b, kv, log, reps: int = 3):
+    """Time aug_kv_resume of the batch's resumed requests and aug_kv_park of
+    the requests it parks (HIP events on the launch stream, mean of `reps`),
+    and a plain hipMemcpyAsync between pinned host memory and the device of
+    the same byte counts for comparison."""
+    import torch
+    pk = b.park
+    dev = kv.k_cache.device
+    stream = torch.cuda.current_stream(dev)
+    res_ids = np.asarray(pk.resume_blocks, np.int32)
+    src_ids = np.asarray(pk.resume_src_blocks, np.int32)
+    park_ids = np.asarray(pk.park_blocks if len(pk.park_blocks) else pk.resume_src_blocks, np.int32)
+    res_dev = torch.from_numpy(res_ids).to(dev)
+    src_dev = torch.from_numpy(src_ids).to(dev)
+    park_dev = torch.from_numpy(park_ids).to(dev)
+    img = kv.host_buffer(len(src_ids))
+    kv.park(src_ids, src_dev, img)            # the parked image the resume reads back
+    out = kv.host_buffer(len(park_ids))
+    torch.cuda.synchronize()
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / reps
+
+    res_bytes = len(res_ids) * kv.record_bytes
+    park_bytes = len(park_ids) * kv.record_bytes
+    t_res = timed(lambda: kv.resume(res_ids, res_dev, img))
+    t_park = timed(lambda: kv.park(park_ids, park_dev, out))
+    d_buf = torch.empty(max(res_bytes, park_bytes), dtype=torch.uint8, device=dev)
+    t_h2d = timed(lambda: d_buf[:res_bytes].copy_(img[:res_bytes], non_blocking=True))
+    t_d2h = timed(lambda: out[:park_bytes].copy_(d_buf[:park_bytes], non_blocking=True))
+    r = {"resume_blocks": int(len(res_ids)), "resume_bytes": int(res_bytes),
+         "resume_gbs": round(res_bytes / t_res / 1e9, 2),
+         "park_blocks": int(len(park_ids)), "park_bytes": int(park_bytes),
+         "park_gbs": round(park_bytes / t_park / 1e9, 2),
+         "h2d_copy_gbs": round(res_bytes / t_h2d / 1e9, 2), "d2h_copy_gbs": round(park_bytes / t_d2h / 1e9, 2),
+         "pcie_peak_gbs": PCIE_PEAK_GBS, "reps": reps}
+    log(f"park/resume: {r}")
+    return r
 
 
 def make_workload(name: str, seed: int, log):
@@ -292,6 +346,8 @@ def main():
                     help="copies of the KV pool used in turn (0: enough for 1 GiB of KV reads between "
                          "two uses of one copy, at most 8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-park-resume", action="store_true",
+                    help="skip the separate park/resume timing of workloads that move paused requests")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--sweep-batches", type=int, default=200,
                     help="budget-sweep-fp8: formed batches replayed per budget")
@@ -438,6 +494,8 @@ def main():
                    "kv_split_tokens": int(info.kv_split_tokens), "seed": args.seed, "pool_copies": n_copies},
         "roofline": roof,
     }
+    if getattr(b, "park", None) is not None and len(b.park.resume_blocks) and not args.no_park_resume:
+        result["park_resume"] = park_resume_rates(b, kv, log)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(b, args.cpu_budget_s)
