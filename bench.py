@@ -2,7 +2,8 @@
 
 A step is one pass of the hot path over one batch: the host batch former
 (token budget, cost, priority, greedy packing), the host planner, the
-upload of the work list, and the attention launch(es) over the paged cache.
+upload of the work list, the append of the step's new K/V rows to the paged
+cache, and the attention launch(es) over it.
 Inputs are synthetic, seeded, and resident in HBM before timing starts.
 Workloads that move paused requests (mixed-8b, long-context-8b) also time
 their resume and park on their own, after the steps, and report them in
@@ -64,6 +65,21 @@ def prefill_flops(b) -> float:
     # rows j attend pos_j + 1 keys: sum = q*(ctx-q) + q(q+1)/2
     keys = (q * (ctx - q) + q * (q + 1) // 2)[pre]
     return float(4 * b.head_dim * b.num_q_heads * keys.sum())
+
+
+def append_bytes(b, info) -> float:
+    """Algorithmic bytes of one append: every new row's K and V read once in
+    the caller's format and written once in the cache's, per KV head; for fp8
+    caches one scale read and written per (block, KV head, K|V); the append
+    list and block ids. Re-encoding earlier tokens when a scale grows depends
+    on the data and is not counted."""
+    row_in = 4 if b.kv_dtype == "f32" else 2
+    row_out = {"f32": 4, "bf16": 2, "fp8": 1}[b.kv_dtype]
+    n = float(b.total_q) * b.num_kv_heads * b.head_dim * 2 * (row_in + row_out)
+    items = int(info.num_append_items)
+    if b.kv_dtype == "fp8":
+        n += items * b.num_kv_heads * 2 * 8
+    return n + items * (16 + 4)
 
 
 def measured_traffic(workload_name: str):
@@ -401,6 +417,14 @@ def main():
     out = torch.empty((b.total_q, b.num_q_heads, b.head_dim),
                       dtype=torch.float32 if b.out_dtype == "f32" else torch.bfloat16, device=dev)
     ev = []
+    ev_append = []
+    # the step's new K/V rows, written into the pool ahead of its attention
+    new_std = 1.0 / np.sqrt(b.head_dim) if WORKLOADS[args.workload] != 1 else 1.0
+    k_new_h, v_new_h = synth.make_new_kv(b, seed=args.seed + 7, std=new_std)
+    new_dt = "f32" if b.kv_dtype == "f32" else "bf16"
+    k_new = rt.to_device_array(k_new_h, new_dt, dev)
+    v_new = rt.to_device_array(v_new_h, new_dt, dev)
+    del k_new_h, v_new_h
 
     def step(i, timed):
         now = 1.0 + 0.02 * i
@@ -426,13 +450,18 @@ def main():
         plan_ev[slot].record(stream)
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
+        a0 = torch.cuda.Event(enable_timing=True)
         kc, vc, ksc, vsc = pools[i % len(pools)]
+        a0.record(stream)
+        aug.aug_kv_append(shape, info, plan_dev, k_new, v_new, kc, vc, ksc, vsc, bids, kv.num_pool_blocks,
+                          stream=stream.cuda_stream)
+        e0.record(stream)
         aug.aug_attn_mixed(shape, info, plan_dev, q, kc, vc, ksc, vsc,
                            bids, kv.num_pool_blocks, out, ws_dev, stream=stream.cuda_stream)
         e1.record(stream)
         if timed:
             ev.append((e0, e1))
+            ev_append.append((a0, e0))
         return info
 
     if args.copy_probe_mib > 0:
@@ -494,6 +523,14 @@ def main():
                    "kv_split_tokens": int(info.kv_split_tokens), "seed": args.seed, "pool_copies": n_copies},
         "roofline": roof,
     }
+    app_ms = np.array([a.elapsed_time(c) for a, c in ev_append])
+    app_bytes = append_bytes(b, info)
+    result["kv_append"] = {
+        "kernel": "aug_kv_append (the step's new K/V rows into the pool, before attention)",
+        "algorithmic_bytes_per_launch": int(app_bytes), "launch_ms": round(float(app_ms.mean()), 4),
+        "launch_ms_median": round(float(np.median(app_ms)), 4),
+        "gbs": round(app_bytes / (float(app_ms.mean()) * 1e-3) / 1e9, 1),
+        "frac_hbm": round(app_bytes / (float(app_ms.mean()) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     if getattr(b, "park", None) is not None and len(b.park.resume_blocks) and not args.no_park_resume:
         result["park_resume"] = park_resume_rates(b, kv, log)
     if not args.no_cpu_baseline:

@@ -121,6 +121,8 @@ typedef struct {
   int32_t total_rows;        /* q_start[num_reqs] */
   int32_t num_reqs;
   int32_t num_tile_merge_groups;
+  int32_t num_append_items;  /* blocks that receive new K/V rows (aug_kv_append) */
+  int32_t reserved;
 } aug_attn_plan_info;
 
 /* Validate a formed batch and write its work list ("plan image") to
@@ -130,9 +132,13 @@ typedef struct {
  * aug_attn_mixed with the same `info`. kv_split_tokens <= 0 lets the planner
  * choose the decode split (keys per work item); a positive value is rounded
  * up to a multiple of block_size. Pure host code; deterministic.
+ * The image also lists the blocks that receive the step's new K/V rows
+ * (info->num_append_items), for aug_kv_append.
  * Errors: AUG_ERR_INVALID (shape, monotonicity, ctx_len < q_len, too few
- * blocks, block id outside the pool), AUG_ERR_UNSUPPORTED (dtype set,
- * head_dim, block_size), AUG_ERR_NO_SPACE (plan_cap < plan_bytes). */
+ * blocks, block id outside the pool; with the host block table, a block that
+ * would receive new tokens of two requests or twice from one),
+ * AUG_ERR_UNSUPPORTED (dtype set, head_dim, block_size), AUG_ERR_NO_SPACE
+ * (plan_cap < plan_bytes). */
 aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batch,
                          int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
                          aug_attn_plan_info* info);
@@ -166,6 +172,34 @@ aug_status aug_attn_mixed(const aug_attn_shape* shape, const aug_attn_plan_info*
                           const void* v_cache, const float* k_scale, const float* v_scale,
                           const int32_t* block_ids, int32_t num_pool_blocks, void* out,
                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Append the step's new K/V rows to the paged cache, before the attention of
+ * the same step reads them: every query row is a token the forward pass
+ * produced (the chunk or decode token scheduled in Algorithm 1, step (5)).
+ * Row j of request r sits at position ctx_len[r] - q_len + j, slot
+ * (position mod block_size) of block block_ids[bt_start[r] + position /
+ * block_size], for every KV head. Device memory:
+ *   plan_dev   the plan image of aug_attn_plan for this batch (read only)
+ *   k_new,     [total_rows][num_kv_heads][head_dim]: float32 for f32 caches,
+ *   v_new      bf16 for bf16 and fp8 caches; finite values
+ *   k_cache, v_cache, k_scale, v_scale, block_ids  as for aug_attn_mixed;
+ *              written in place
+ * f32 and bf16 caches receive the rows unchanged. fp8 E4M3FN caches (one
+ * float32 scale per block and KV head, value = code * scale): per block and
+ * KV head that receives tokens, with a = max |x| of the new tokens, the scale
+ * becomes a / 448 if the request's first new token lands in slot 0, else
+ * max(old scale, a / 448); when it grows, the block's earlier codes are
+ * re-encoded as enc(dec(code) * old / new); new tokens are enc(x / scale)
+ * (0 if the scale is 0). enc rounds to nearest even and saturates at +-448;
+ * products and quotients are single float32 operations in that order.
+ * A block id outside the pool is skipped. Enqueued on `stream` as one kernel
+ * launch (none for an empty batch).
+ * Errors: AUG_ERR_INVALID (NULL pointers, info/shape mismatch,
+ * missing scales for fp8), AUG_ERR_HIP (launch). */
+aug_status aug_kv_append(const aug_attn_shape* shape, const aug_attn_plan_info* info,
+                         const void* plan_dev, const void* k_new, const void* v_new, void* k_cache,
+                         void* v_cache, float* k_scale, float* v_scale, const int32_t* block_ids,
+                         int32_t num_pool_blocks, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Park / resume (Swap policy: swap-out during an external call, swap-in     */

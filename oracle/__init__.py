@@ -7,6 +7,7 @@ definitions they cite, that the HIP library is checked against:
 * ``attention`` - paged, GQA, causal attention over materialised K/V (numpy, float64)
 * ``brute``     - the same attention as scalar Python loops (tiny shapes only)
 * ``kvpark``    - the byte image of parked KV blocks, and the resume scatter
+* ``kvappend``  - the step's new K/V rows written into the paged cache
 * ``former``    - the token-budget batch former (pure Python, float64)
 
 Only the test suite, the smoke check and the benchmark's CPU-baseline leg

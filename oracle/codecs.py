@@ -43,3 +43,27 @@ def storage_to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "fp8":
         return e4m3fn_bits_to_f64(x)
     raise ValueError(dtype)
+
+
+# Finite non-negative E4M3FN values in code order (codes 0x00 .. 0x7E); the
+# value grows with the code, so nearest-value search is a sorted search.
+_POS_VALUES = E4M3FN_TABLE[:0x7F]
+
+
+def e4m3fn_encode(y: np.ndarray) -> np.ndarray:
+    """float32 -> E4M3FN codes: the nearest finite value, ties to the code with
+    an even mantissa (round to nearest even), magnitudes beyond 448 saturate
+    to +-448, the sign of zero is kept. Found by searching the value table,
+    not by manipulating bits."""
+    y = np.asarray(y, dtype=np.float32).astype(np.float64)
+    a = np.minimum(np.abs(y), 448.0)
+    hi = np.searchsorted(_POS_VALUES, a, side="left")          # first value >= a
+    hi = np.minimum(hi, 0x7E)
+    lo = np.maximum(hi - 1, 0)
+    d_lo = a - _POS_VALUES[lo]
+    d_hi = _POS_VALUES[hi] - a
+    pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (hi % 2 == 0))
+    code = np.where(pick_hi, hi, lo)
+    code = np.where(a == _POS_VALUES[hi], hi, code)             # exact hits
+    sign = np.signbit(y)
+    return (code | (sign.astype(np.int64) << 7)).astype(np.uint8)

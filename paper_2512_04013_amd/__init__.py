@@ -30,7 +30,7 @@ AUG_POL_NONE, AUG_PRESERVE, AUG_DISCARD, AUG_SWAP = 0, 1, 2, 3
 
 DTYPE_CODES = {"f32": AUG_F32, "bf16": AUG_BF16, "fp8": AUG_FP8_E4M3FN}
 
-EXPORTED = ["aug_attn_plan", "aug_attn_mixed", "aug_kv_record_bytes", "aug_kv_park",
+EXPORTED = ["aug_attn_plan", "aug_attn_mixed", "aug_kv_append", "aug_kv_record_bytes", "aug_kv_park",
             "aug_kv_resume", "aug_form_batch", "aug_status_string", "aug_last_error",
             "aug_abi_version"]
 
@@ -60,7 +60,8 @@ class aug_attn_plan_info(C.Structure):
                 ("num_prefill_items", C.c_int32), ("num_merge_groups", C.c_int32),
                 ("num_partials", C.c_int32), ("kv_split_tokens", C.c_int32),
                 ("total_rows", C.c_int32), ("num_reqs", C.c_int32),
-                ("num_tile_merge_groups", C.c_int32)]
+                ("num_tile_merge_groups", C.c_int32), ("num_append_items", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class aug_request(C.Structure):
@@ -116,6 +117,8 @@ def lib():
                                 C.c_size_t, C.POINTER(aug_attn_plan_info)]
     L.aug_attn_mixed.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P,
                                  P, P, P, C.c_int32, P, P, C.c_size_t, P]
+    L.aug_kv_append.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P, P,
+                                P, P, P, C.c_int32, P]
     L.aug_kv_record_bytes.argtypes = [C.POINTER(aug_attn_shape)]
     L.aug_kv_record_bytes.restype = C.c_size_t
     L.aug_kv_park.argtypes = [C.POINTER(aug_attn_shape), P, P, P, P, P, P, C.c_int32, C.c_int32, P,
@@ -124,7 +127,8 @@ def lib():
                                 C.c_size_t, P, C.c_size_t, P]
     L.aug_form_batch.argtypes = [P, C.c_int32, C.c_int64, C.c_double, C.POINTER(aug_former_params),
                                  C.POINTER(aug_batch_plan)]
-    for f in ("aug_attn_plan", "aug_attn_mixed", "aug_kv_park", "aug_kv_resume", "aug_form_batch"):
+    for f in ("aug_attn_plan", "aug_attn_mixed", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
+              "aug_form_batch"):
         getattr(L, f).restype = C.c_int
     L.aug_status_string.argtypes = [C.c_int]
     L.aug_status_string.restype = C.c_char_p
@@ -229,6 +233,16 @@ def aug_attn_mixed(shape: aug_attn_shape, info: aug_attn_plan_info, plan_dev, q,
                                 _ptr(k_cache), _ptr(v_cache), _ptr(k_scale), _ptr(v_scale),
                                 _ptr(block_ids), int(num_pool_blocks), _ptr(out), _ptr(workspace),
                                 int(workspace_bytes), st), "aug_attn_mixed")
+
+
+def aug_kv_append(shape: aug_attn_shape, info: aug_attn_plan_info, plan_dev, k_new, v_new, k_cache,
+                  v_cache, k_scale, v_scale, block_ids, num_pool_blocks: int, stream=None):
+    """Enqueue the write of the planned batch's new K/V rows into the pool
+    (all device arguments are torch tensors or raw device addresses)."""
+    st = _stream(stream, k_new, k_cache)
+    _check(lib().aug_kv_append(C.byref(shape), C.byref(info), _ptr(plan_dev), _ptr(k_new), _ptr(v_new),
+                               _ptr(k_cache), _ptr(v_cache), _ptr(k_scale), _ptr(v_scale),
+                               _ptr(block_ids), int(num_pool_blocks), st), "aug_kv_append")
 
 
 # ---- park / resume -------------------------------------------------------------------

@@ -1062,9 +1062,8 @@ extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_pla
   if (!info) return aug::fail(AUG_ERR_INVALID, "%s: info is NULL", who);
   if (info->num_items < 0 || info->num_merge_groups < 0 || info->num_partials < 0 ||
       info->num_tile_merge_groups < 0 || info->num_tile_merge_groups > info->num_merge_groups ||
-      info->plan_bytes != static_cast<int64_t>(sizeof(aug::PlanHeader)) +
-                              static_cast<int64_t>(info->num_items) * sizeof(WorkItem) +
-                              static_cast<int64_t>(info->num_merge_groups) * (sizeof(MergeGroup) + 4))
+      info->num_append_items < 0 ||
+      info->plan_bytes != aug::plan_image_bytes(info->num_items, info->num_merge_groups, info->num_append_items))
     return aug::fail(AUG_ERR_INVALID, "%s: info is inconsistent", who);
   if (info->num_items == 0) return AUG_OK;
   if (!plan_dev || !q || !k_cache || !v_cache || !block_ids || !out)

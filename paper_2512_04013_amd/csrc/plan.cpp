@@ -149,6 +149,28 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   if (total_rows > (int64_t{1} << 30))
     return fail(AUG_ERR_UNSUPPORTED, "%s: %lld rows", who, (long long)total_rows);
 
+  // blocks that receive this step's new K/V rows (aug_kv_append); with the
+  // host block table, no block may receive tokens of two requests (or twice
+  // from one), which concurrent appends could not merge
+  int64_t n_append = 0;
+  for (int32_t r = 0; r < n; ++r) {
+    const int64_t first = b->ctx_len[r] - (b->q_start[r + 1] - b->q_start[r]);
+    n_append += (b->ctx_len[r] - 1) / kBlock - first / kBlock + 1;
+  }
+  if (b->block_ids && n_append > 0) {
+    std::vector<int32_t> touched;
+    touched.reserve(static_cast<size_t>(n_append));
+    for (int32_t r = 0; r < n; ++r) {
+      const int64_t first = b->ctx_len[r] - (b->q_start[r + 1] - b->q_start[r]);
+      for (int64_t blk = first / kBlock; blk <= (b->ctx_len[r] - 1) / kBlock; ++blk)
+        touched.push_back(b->block_ids[b->bt_start[r] + blk]);
+    }
+    std::sort(touched.begin(), touched.end());
+    const auto dup = std::adjacent_find(touched.begin(), touched.end());
+    if (dup != touched.end())
+      return fail(AUG_ERR_INVALID, "%s: block %d receives new tokens more than once", who, *dup);
+  }
+
   const int32_t split = choose_split(total_row_keys, kv_split_tokens);
   const int32_t pos_per_tile = kTileRows / g;
   const int32_t kv_bytes_all = s->kv_dtype == AUG_F32 ? 4 : s->kv_dtype == AUG_BF16 ? 2 : 1;
@@ -297,7 +319,8 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   if (n_parts > (int64_t{1} << 30))
     return fail(AUG_ERR_UNSUPPORTED, "%s: %lld split-K partials", who, (long long)n_parts);
   const int64_t counters_off = groups_off + n_groups * static_cast<int64_t>(sizeof(MergeGroup));
-  const int64_t plan_bytes = counters_off + n_groups * 4;
+  const int64_t append_off = append_offset(n_items, n_groups);
+  const int64_t plan_bytes = plan_image_bytes(n_items, n_groups, n_append);
   if (plan_bytes > INT32_MAX)
     return fail(AUG_ERR_UNSUPPORTED, "%s: plan image of %lld bytes", who, (long long)plan_bytes);
   const int64_t ws = ((n_parts * partial_floats(g, s->head_dim) * 4 + 255) / 256) * 256;
@@ -313,6 +336,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   info->total_rows = static_cast<int32_t>(total_rows);
   info->num_reqs = n;
   info->num_tile_merge_groups = static_cast<int32_t>(tile_groups.size());
+  info->num_append_items = static_cast<int32_t>(n_append);
   if (!plan_host) return AUG_OK;
   if (plan_cap < static_cast<size_t>(plan_bytes))
     return fail(AUG_ERR_NO_SPACE, "%s: plan buffer %zu < %lld bytes", who, plan_cap,
@@ -331,6 +355,8 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   hdr.items_offset = static_cast<int32_t>(items_off);
   hdr.groups_offset = static_cast<int32_t>(groups_off);
   hdr.counters_offset = static_cast<int32_t>(counters_off);
+  hdr.append_offset = static_cast<int32_t>(append_off);
+  hdr.num_append_items = static_cast<int32_t>(n_append);
   std::memcpy(base, &hdr, sizeof(hdr));
   auto* items = reinterpret_cast<WorkItem*>(base + items_off);
   auto* groups = reinterpret_cast<MergeGroup*>(base + groups_off);
@@ -377,6 +403,18 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
     }
   }
   emit_tiles_longer_than(-1.0);
-  std::memset(base + counters_off, 0, static_cast<size_t>(n_groups) * 4);
+  std::memset(base + counters_off, 0, static_cast<size_t>(append_off - counters_off));
+  auto* app = reinterpret_cast<AppendItem*>(base + append_off);
+  int64_t na = 0;
+  for (int32_t r = 0; r < n; ++r) {
+    const int32_t first = b->ctx_len[r] - (b->q_start[r + 1] - b->q_start[r]);
+    for (int32_t p = first; p < b->ctx_len[r];) {
+      const int32_t blk = p / kBlock;
+      const int32_t end = std::min(b->ctx_len[r], (blk + 1) * kBlock);
+      app[na++] = AppendItem{b->q_start[r] + (p - first), static_cast<int16_t>(end - p),
+                             static_cast<int16_t>(p % kBlock), b->bt_start[r] + blk, 0};
+      p = end;
+    }
+  }
   return AUG_OK;
 }

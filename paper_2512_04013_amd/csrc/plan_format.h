@@ -7,7 +7,7 @@
 namespace aug {
 
 constexpr int32_t kPlanMagic = 0x4E4C5041;  // "APLN"
-constexpr int32_t kPlanVersion = 1;
+constexpr int32_t kPlanVersion = 2;
 constexpr int32_t kBlock = 16;              // tokens per KV block
 constexpr int32_t kKeyTile = 64;            // keys per MFMA tile (4 blocks)
 constexpr int32_t kTileRows = 128;          // query rows (positions x group heads) per MFMA tile
@@ -31,7 +31,9 @@ struct PlanHeader {          // 64 bytes
   int32_t items_offset;      // bytes from the start of the image
   int32_t groups_offset;
   int32_t counters_offset;   // int32 per merge group, zero in the image
-  int32_t reserved[5];
+  int32_t append_offset;     // AppendItem list (16-byte aligned)
+  int32_t num_append_items;
+  int32_t reserved[3];
 };
 
 struct WorkItem {            // 48 bytes
@@ -61,9 +63,32 @@ struct MergeGroup {          // 16 bytes
   int32_t n_parts;
 };
 
+// One block that receives new tokens of the step: rows q_row0 .. q_row0 +
+// n_rows - 1 of Q (and of the new K/V rows) go to slots slot0 .. slot0 +
+// n_rows - 1 of block block_ids[bt_index]; slot0 == 0 means the block holds
+// nothing of the request yet.
+struct AppendItem {          // 16 bytes
+  int32_t q_row0;
+  int16_t n_rows;
+  int16_t slot0;
+  int32_t bt_index;
+  int32_t reserved;
+};
+
 static_assert(sizeof(PlanHeader) == 64, "plan header layout");
+static_assert(sizeof(AppendItem) == 16, "append item layout");
 static_assert(sizeof(WorkItem) == 48, "work item layout");
 static_assert(sizeof(MergeGroup) == 16, "merge group layout");
+
+// Layout of the image: header, work items, merge groups, one int32 counter
+// per merge group, then (16-byte aligned) the append items.
+constexpr int64_t append_offset(int64_t num_items, int64_t num_groups) {
+  return ((static_cast<int64_t>(sizeof(PlanHeader)) + num_items * static_cast<int64_t>(sizeof(WorkItem)) +
+           num_groups * static_cast<int64_t>(sizeof(MergeGroup) + 4) + 15) / 16) * 16;
+}
+constexpr int64_t plan_image_bytes(int64_t num_items, int64_t num_groups, int64_t num_append) {
+  return append_offset(num_items, num_groups) + num_append * static_cast<int64_t>(sizeof(AppendItem));
+}
 
 // Split-K partial of one (row, KV head, key span): unnormalised o[G][D]
 // relative to the running maximum, then m[G] (log2 domain) and l[G], padded to

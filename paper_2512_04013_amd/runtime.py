@@ -10,7 +10,7 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from . import (aug_attn_mixed, aug_attn_plan, aug_kv_park, aug_kv_record_bytes, aug_kv_resume,
+from . import (aug_attn_mixed, aug_attn_plan, aug_kv_append, aug_kv_park, aug_kv_record_bytes, aug_kv_resume,
                make_shape)
 
 _TORCH_STORAGE = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.uint8}
@@ -81,6 +81,18 @@ class MixedAttention:
                        self.kv.k_scale, self.kv.v_scale, self.block_ids, self.kv.num_pool_blocks,
                        self.out, self.workspace, stream=stream)
         return self.out
+
+    def append(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
+        """Write the batch's new K/V rows ([rows][H_kv][D]) into the pool."""
+        want = (int(self.info.total_rows), self.shape.num_kv_heads, self.shape.head_dim)
+        dtype = torch.float32 if self.shape.kv_dtype == 0 else torch.bfloat16
+        for t in (k_new, v_new):
+            if tuple(t.shape) != want or t.dtype != dtype or not t.is_contiguous():
+                raise ValueError(f"new K/V rows must be contiguous {dtype} of shape {want}, got "
+                                 f"{t.dtype} {tuple(t.shape)}")
+        aug_kv_append(self.shape, self.info, self.plan_dev, k_new, v_new, self.kv.k_cache,
+                      self.kv.v_cache, self.kv.k_scale, self.kv.v_scale, self.block_ids,
+                      self.kv.num_pool_blocks, stream=stream)
 
 
 def shape_of(batch) -> object:

@@ -17,6 +17,8 @@ from .attn_inputs import (  # noqa: F401
     make_mixed_8b,
     make_long_context,
     make_batch_from_lengths,
+    make_new_kv,
+    poison_new_slots,
     round_to_bf16_bits,
     encode_e4m3fn_bits,
     BF16_NAN,

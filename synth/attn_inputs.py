@@ -318,6 +318,34 @@ def make_batch_from_lengths(
 # the five workloads
 # ---------------------------------------------------------------------------
 
+def make_new_kv(batch: AttnBatch, seed: int, std: float = 1.0):
+    """The step's new K and V rows, each [total_q, H_kv, D] drawn N(0, std^2):
+    float32 for f32 caches, bf16 bit patterns for bf16 and fp8 caches (an fp8
+    cache receives bf16 rows and encodes them itself)."""
+    rng = np.random.default_rng(seed)
+    shape = (batch.total_q, batch.num_kv_heads, batch.head_dim)
+    dt = "f32" if batch.kv_dtype == "f32" else "bf16"
+    k = _to_storage(rng.standard_normal(shape, dtype=np.float32) * np.float32(std), dt)
+    v = _to_storage(rng.standard_normal(shape, dtype=np.float32) * np.float32(std), dt)
+    return k, v
+
+
+def poison_new_slots(batch: AttnBatch, copy: bool = True) -> AttnBatch:
+    """``batch`` (a copy unless ``copy`` is False) whose slots at this step's
+    query positions (the ones an append fills) hold the NaN poison, as before
+    the step's K/V exist. Scales are left as they are."""
+    out = dataclasses.replace(batch, k_cache=batch.k_cache.copy(), v_cache=batch.v_cache.copy()) \
+        if copy else batch
+    nan = {"f32": F32_NAN, "bf16": BF16_NAN, "fp8": FP8_NAN}[batch.kv_dtype]
+    q_len = batch.q_len
+    for r in range(batch.num_reqs):
+        blocks = batch.blocks_of(r)
+        for p in range(int(batch.ctx_len[r]) - int(q_len[r]), int(batch.ctx_len[r])):
+            out.k_cache[blocks[p // BLOCK], :, p % BLOCK, :] = nan
+            out.v_cache[blocks[p // BLOCK], :, p % BLOCK, :] = nan
+    return out
+
+
 def _lognormal_ctx(rng, n, median, sigma, lo, hi):
     x = np.rint(rng.lognormal(np.log(median), sigma, size=n))
     return np.clip(x, lo, hi).astype(np.int64)

@@ -36,7 +36,7 @@ def _shape(b):
 
 def _decode_plan(plan):
     hdr = plan[:64].view(np.int32)
-    assert hdr[0] == 0x4E4C5041 and hdr[1] == 1
+    assert hdr[0] == 0x4E4C5041 and hdr[1] == 2
     n_items, n_groups = hdr[2], hdr[4]
     item_t = np.dtype([("kvh", "<i2"), ("kind", "i1"), ("res", "i1"), ("q_row0", "<i4"),
                        ("n_rows", "<i2"), ("stride", "<i2"), ("kb", "<i4"), ("ke", "<i4"),
@@ -46,7 +46,10 @@ def _decode_plan(plan):
     items = plan[hdr[8]:hdr[8] + 48 * n_items].view(item_t)
     groups = plan[hdr[9]:hdr[9] + 16 * n_groups].view(np.int32).reshape(-1, 4)
     counters = plan[hdr[10]:hdr[10] + 4 * n_groups].view(np.int32)
-    assert hdr[10] == hdr[9] + 16 * n_groups and hdr[10] + 4 * n_groups == len(plan)
+    assert hdr[10] == hdr[9] + 16 * n_groups
+    # the append list follows the counters, 16-byte aligned, and ends the image
+    assert hdr[11] == (hdr[10] + 4 * n_groups + 15) // 16 * 16 and hdr[11] + 16 * hdr[12] == len(plan)
+    assert not plan[hdr[10] + 4 * n_groups:hdr[11]].any()
     assert not counters.any(), "completion counters start at zero"
     return hdr, items, groups
 
