@@ -208,7 +208,8 @@ def make_workload(name: str, seed: int, log):
     from paper_2512_04013_amd import runtime as rt
     budget = 8192
     t0 = time.time()
-    run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), seed=seed)
+    run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), rt.serving_lifecycle(),
+                           seed=seed)
     pick = sweep.select_steps(run.steps, 0, seed)["most_prefill" if name == "sweep-prefill-fp8" else "most_context"]
     log(f"trace served under budget {budget}: {len(run.steps)} batches in {time.time() - t0:.1f} s; "
         f"batch {pick} chosen")
@@ -233,7 +234,8 @@ def budget_sweep(args, log):
     runs = {}
     for budget in sweep.BUDGETS:
         t0 = time.time()
-        run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), seed=args.seed,
+        run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), rt.serving_lifecycle(),
+                               seed=args.seed,
                                max_steps=4000 if budget == 256 else 40_000)
         n = len(run.steps)
         pick = sorted(set(np.linspace(0, n - 1, min(n, args.sweep_batches)).astype(int).tolist())

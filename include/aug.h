@@ -6,15 +6,19 @@
  * Augmented LLM Inference Serving" (arXiv 2512.04013) forms, every engine
  * iteration, a batch of requests that are prefilling a prompt, prefilling the
  * tokens an external call returned, recomputing a discarded context, or
- * decoding (request lifecycle, Eq. 1; Algorithm 1, steps (3)-(5)). Requests
+ * decoding (request lifecycle, Eq. 1; Algorithm 1, steps (1)-(5)). Requests
  * paused on an external call keep their KV cache on the GPU, park it in host
  * memory, or discard it (context-handling policies, Appendix B). This library
  * runs the data-parallel work of one such iteration:
  *
+ *   aug_request_arrive, aug_request_return
+ *                     host: a request's record on arrival and on the return
+ *                     of an external call (Algorithm 1, steps (1)-(2))
  *   aug_form_batch    host: token budget (Eq. token), cost and priority
  *                     (Eqs. cost, c_fb, c_ik_new, value, theta), Waste policy
  *                     choice (Appendix B) and greedy packing (Algorithm 1 (4))
  *   aug_attn_plan     host: validates a formed batch and writes the work list
+ *   aug_kv_append     device: the step's new K/V rows into their paged slots
  *   aug_attn_mixed    device: one launch of paged, causal, grouped-query
  *                     attention over every chunked-prefill row and decode row
  *                     of the batch (plus a merge launch for split prefill tiles)
@@ -47,7 +51,7 @@ extern "C" {
 typedef enum {
   AUG_OK = 0,
   AUG_ERR_INVALID = -1,      /* an argument is out of its documented range */
-  AUG_ERR_UNSUPPORTED = -2,  /* a valid combination this build does not run */
+  AUG_ERR_UNSUPPORTED = -2,  /* a valid combination the library does not run */
   AUG_ERR_NO_SPACE = -3,     /* a caller buffer is too small */
   AUG_ERR_HIP = -4           /* the HIP runtime reported an error */
 } aug_status;
@@ -60,6 +64,13 @@ typedef enum { AUG_WAITING = 0, AUG_RUNNING = 1, AUG_SWAPPED = 2, AUG_PAUSED = 3
 /* Context-handling policies (set Pi), in the order the paper lists them in
  * the Waste minimisation of Appendix B; that order breaks ties. */
 typedef enum { AUG_POL_NONE = 0, AUG_PRESERVE = 1, AUG_DISCARD = 2, AUG_SWAP = 3 } aug_policy;
+
+/* Ranking of the candidates in Algorithm 1, step (4). THETA is the paper's
+ * value density theta = (1 + beta w) / C (Eqs. value, theta); FCFS (arrival
+ * order) is the scheduling of the systems the paper starts from, and SSJF
+ * (shortest predicted output first) the prediction-based baseline of its
+ * evaluation. Ties: earlier arrival, then smaller id. */
+typedef enum { AUG_ORDER_THETA = 0, AUG_ORDER_FCFS = 1, AUG_ORDER_SSJF = 2 } aug_order;
 
 /* ------------------------------------------------------------------------ */
 /* Attention                                                                 */
@@ -279,6 +290,8 @@ typedef struct {
   int32_t chunk_cap;      /* most prefill tokens one request takes per iteration */
   int32_t block_size;     /* tokens per pool block */
   int32_t skip_instead_of_break; /* 0: stop at the first request that does not fit */
+  int32_t order;          /* aug_order of the ranking */
+  int32_t reserved;
 } aug_former_params;
 
 /* Output of aug_form_batch. The caller sets `cap` and the array pointers; each
@@ -309,6 +322,34 @@ typedef struct {
  * AUG_ERR_NO_SPACE (more than `cap` entries in any output list). */
 aug_status aug_form_batch(const aug_request* reqs, int32_t n, int64_t free_blocks, double now,
                           const aug_former_params* params, aug_batch_plan* out);
+
+/* Algorithm 1, step (1): a new request enters the waiting queue. Fills every
+ * field of *r: the first segment prefills the prompt (seg 1, seg_ctx 0,
+ * seg_prefill = pending = prompt_tokens, no KV held), with the predictor's
+ * output length and call duration (pred_call 0 and has_next_call 0 when the
+ * request makes no call). Its policy, cost and priority are evaluated by
+ * aug_form_batch at every iteration, since the waiting time w changes.
+ * Errors: AUG_ERR_INVALID (NULL r, prompt_tokens < 1, pred_out < 1,
+ * pred_call < 0 or not finite). */
+aug_status aug_request_arrive(aug_request* r, int64_t id, double arrival, int32_t prompt_tokens,
+                              int32_t pred_out, double pred_call, int32_t has_next_call);
+
+/* Algorithm 1, step (2): a paused request's external call has returned.
+ * `realised` is the policy actually executed during the wait (p_{i,k-1}):
+ * PRESERVE (its KV stayed on the GPU), SWAP (its blocks were parked) or
+ * DISCARD (its blocks were freed). The next segment starts at the request's
+ * full context `context_tokens` (prompt, generated and returned tokens so
+ * far) and prefills the `ret_tokens` the call returned; its cost from then on
+ * is the feedback cost C^fb (Eq. c_fb) plus decode and next-call terms. The
+ * request is requeued by the realised policy: PRESERVE -> running, SWAP ->
+ * swapped (pending = ret_tokens), DISCARD -> waiting with no KV and pending =
+ * context_tokens + ret_tokens (recompute). The predictions are those of the
+ * new segment.
+ * Errors: AUG_ERR_INVALID (NULL r, r not PAUSED, unknown policy,
+ * context_tokens < ctx_len, ret_tokens < 0, pred_out < 1, pred_call < 0 or
+ * not finite). */
+aug_status aug_request_return(aug_request* r, int32_t realised, int32_t context_tokens, int32_t ret_tokens,
+                              int32_t pred_out, double pred_call, int32_t has_next_call);
 
 /* ------------------------------------------------------------------------ */
 

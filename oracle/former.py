@@ -41,11 +41,21 @@ design notes):
 * ties in theta go to the earlier arrival, then the smaller id;
 * a request also needs ceil((ctx + tokens) / block) pool blocks beyond those
   it holds (all of them if swapped out); if free plus reclaimable blocks
-  cannot cover it, it counts as not fitting. Blocks are reclaimed lazily from
+  cannot cover it, it is passed over for this iteration and packing goes on
+  (the algorithm's stop is the token-budget test alone; memory enters it
+  through the budget). Blocks are reclaimed lazily from
   paused Swap/Discard requests, longest predicted remaining pause first
   (ties by id): Swap victims are parked, Discard victims are freed;
 * ``skip_instead_of_break`` replaces the stop with a skip (the greedy of the
-  approximation appendix, which adds every request that fits).
+  approximation appendix, which adds every request that fits);
+* ``order`` swaps the ranking key for the baselines the paper compares
+  against: FCFS ranks by arrival, SSJF by the predicted output length of the
+  current segment (shortest first); both break ties like theta does.
+
+Steps (1) and (2) of Algorithm 1 change a request's record: on arrival it
+waits to prefill its prompt in segment 1 (``arrive``); when an external call
+returns, the next segment starts from the realised policy of the wait, which
+decides the queue it rejoins and what it must prefill (``on_return``).
 
 All arithmetic is on Python floats (IEEE binary64) and ints, in a fixed order,
 so the C++ former reproduces it bit for bit.
@@ -59,6 +69,7 @@ from typing import List
 
 WAITING, RUNNING, SWAPPED, PAUSED = 0, 1, 2, 3
 NONE, PRESERVE, DISCARD, SWAP = 0, 1, 2, 3
+ORDER_THETA, ORDER_FCFS, ORDER_SSJF = 0, 1, 2
 
 
 @dataclasses.dataclass
@@ -94,6 +105,7 @@ class Params:
     swap_s_per_tok: float = 2.0e-6
     n_fwd_max: int = 1
     skip_instead_of_break: int = 0
+    order: int = 0                # ORDER_THETA, ORDER_FCFS or ORDER_SSJF
 
 
 @dataclasses.dataclass
@@ -257,7 +269,12 @@ def form_batch(reqs: List[Request], free_blocks: int, block_size: int, now: floa
         return r.pred_call - (now - r.pause_start)
 
     victims.sort(key=lambda i: (-remaining_pause(i), reqs[i].id))
-    ranked = sorted(cands, key=lambda i: (-theta[i], reqs[i].arrival, reqs[i].id))
+    if p.order == ORDER_FCFS:
+        ranked = sorted(cands, key=lambda i: (reqs[i].arrival, reqs[i].id))
+    elif p.order == ORDER_SSJF:
+        ranked = sorted(cands, key=lambda i: (reqs[i].pred_out, reqs[i].arrival, reqs[i].id))
+    else:
+        ranked = sorted(cands, key=lambda i: (-theta[i], reqs[i].arrival, reqs[i].id))
 
     free_now, reclaim_left, vi, active = free_blocks, preempt, 0, 0
     ids, q_len, th, resume_ids, park_ids, free_ids = [], [], [], [], [], []
@@ -271,9 +288,7 @@ def form_batch(reqs: List[Request], free_blocks: int, block_size: int, now: floa
         have = 0 if r.state == SWAPPED else r.blocks_on_gpu
         need = max(0, -(-(r.ctx_len + t) // block_size) - have)
         if need > free_now + reclaim_left:
-            if p.skip_instead_of_break:
-                continue
-            break
+            continue            # no memory for it now: not a budget stop, later ones may fit
         while need > free_now:
             v = reqs[victims[vi]]
             vi += 1
@@ -288,3 +303,35 @@ def form_batch(reqs: List[Request], free_blocks: int, block_size: int, now: floa
         if r.state == SWAPPED:
             resume_ids.append(r.id)
     return Plan(budget, ids, q_len, th, resume_ids, park_ids, free_ids, policy, cost)
+
+
+# ---- Algorithm 1, steps (1) and (2): the request record -------------------------
+
+def arrive(id: int, arrival: float, prompt_tokens: int, pred_out: int, pred_call: float,
+           has_next_call: int) -> Request:
+    """A new request waits to prefill its prompt in its first segment."""
+    return Request(id=id, arrival=arrival, last_sched=-1.0, state=WAITING, seg=1, prev_policy=NONE,
+                   cur_policy=NONE, seg_ctx=0, seg_prefill=prompt_tokens, pred_out=pred_out,
+                   pred_call=pred_call if has_next_call else 0.0, has_next_call=1 if has_next_call else 0,
+                   ctx_len=0, pending=prompt_tokens, blocks_on_gpu=0, pause_start=0.0)
+
+
+def on_return(r: Request, realised: int, context_tokens: int, ret_tokens: int, pred_out: int,
+              pred_call: float, has_next_call: int) -> Request:
+    """The record after the external call of a paused request returned:
+    the next segment starts at the full context and prefills the returned
+    tokens; the realised policy of the wait decides the queue (Preserve:
+    running; Swap: swapped; Discard: waiting, recomputing the whole context)."""
+    assert r.state == PAUSED
+    out = dataclasses.replace(r, seg=r.seg + 1, prev_policy=realised, cur_policy=NONE,
+                              seg_ctx=context_tokens, seg_prefill=ret_tokens, pred_out=pred_out,
+                              pred_call=pred_call if has_next_call else 0.0,
+                              has_next_call=1 if has_next_call else 0)
+    if realised == PRESERVE:
+        out.state, out.pending = RUNNING, ret_tokens
+    elif realised == SWAP:
+        out.state, out.pending = SWAPPED, ret_tokens
+    else:
+        out.state, out.ctx_len, out.blocks_on_gpu = WAITING, 0, 0
+        out.pending = context_tokens + ret_tokens
+    return out

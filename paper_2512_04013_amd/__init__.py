@@ -30,7 +30,7 @@ AUG_POL_NONE, AUG_PRESERVE, AUG_DISCARD, AUG_SWAP = 0, 1, 2, 3
 
 DTYPE_CODES = {"f32": AUG_F32, "bf16": AUG_BF16, "fp8": AUG_FP8_E4M3FN}
 
-EXPORTED = ["aug_attn_plan", "aug_attn_mixed", "aug_kv_append", "aug_kv_record_bytes", "aug_kv_park",
+EXPORTED = ["aug_request_arrive", "aug_request_return", "aug_attn_plan", "aug_attn_mixed", "aug_kv_append", "aug_kv_record_bytes", "aug_kv_park",
             "aug_kv_resume", "aug_form_batch", "aug_status_string", "aug_last_error",
             "aug_abi_version"]
 
@@ -78,7 +78,7 @@ class aug_former_params(C.Structure):
                 ("t_iter", C.c_double), ("fwd_a", C.c_double), ("fwd_b", C.c_double),
                 ("swap_s_per_tok", C.c_double), ("n_fwd_max", C.c_int64), ("t_max", C.c_int32),
                 ("chunk_cap", C.c_int32), ("block_size", C.c_int32),
-                ("skip_instead_of_break", C.c_int32)]
+                ("skip_instead_of_break", C.c_int32), ("order", C.c_int32), ("reserved", C.c_int32)]
 
 
 class aug_batch_plan(C.Structure):
@@ -127,8 +127,10 @@ def lib():
                                 C.c_size_t, P, C.c_size_t, P]
     L.aug_form_batch.argtypes = [P, C.c_int32, C.c_int64, C.c_double, C.POINTER(aug_former_params),
                                  C.POINTER(aug_batch_plan)]
+    L.aug_request_arrive.argtypes = [P, C.c_int64, C.c_double, C.c_int32, C.c_int32, C.c_double, C.c_int32]
+    L.aug_request_return.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_double, C.c_int32]
     for f in ("aug_attn_plan", "aug_attn_mixed", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
-              "aug_form_batch"):
+              "aug_form_batch", "aug_request_arrive", "aug_request_return"):
         getattr(L, f).restype = C.c_int
     L.aug_status_string.argtypes = [C.c_int]
     L.aug_status_string.restype = C.c_char_p
@@ -275,12 +277,15 @@ def aug_kv_resume(shape, k_cache, v_cache, k_scale, v_scale, block_ids_dev, n_bl
 
 # ---- batch former ----------------------------------------------------------------------
 
+AUG_ORDER_THETA, AUG_ORDER_FCFS, AUG_ORDER_SSJF = 0, 1, 2
+
+
 def former_params(beta=5e-5, t_max=2048, beta_low=0.5, beta_high=2.0, chunk_cap=512, t_iter=0.02,
                   fwd_a=0.015, fwd_b=2.0e-8, swap_s_per_tok=2.0e-6, n_fwd_max=1,
-                  skip_instead_of_break=0, block_size=16) -> aug_former_params:
+                  skip_instead_of_break=0, block_size=16, order=AUG_ORDER_THETA) -> aug_former_params:
     return aug_former_params(beta, beta_low, beta_high, t_iter, fwd_a, fwd_b, swap_s_per_tok,
                              int(n_fwd_max), int(t_max), int(chunk_cap), int(block_size),
-                             int(skip_instead_of_break))
+                             int(skip_instead_of_break), int(order), 0)
 
 
 def aug_form_batch(reqs: np.ndarray, free_blocks: int, now: float, params: aug_former_params):
@@ -308,3 +313,26 @@ def aug_form_batch(reqs: np.ndarray, free_blocks: int, now: float, params: aug_f
                 theta=theta[:k].copy(), resume_ids=res[:out.n_resume].copy(),
                 park_ids=park[:out.n_park].copy(), free_ids=free[:out.n_free].copy(),
                 policy=pol[:n].copy(), cost=cost[:n].copy())
+
+
+# ---- request records (Algorithm 1, steps (1)-(2)) ------------------------------------
+
+def aug_request_arrive(id: int, arrival: float, prompt_tokens: int, pred_out: int, pred_call: float,
+                       has_next_call: int) -> np.ndarray:
+    """The record (one REQUEST_DTYPE element) of a newly arrived request."""
+    rec = np.zeros(1, REQUEST_DTYPE)
+    _check(lib().aug_request_arrive(rec.ctypes.data, int(id), float(arrival), int(prompt_tokens),
+                                    int(pred_out), float(pred_call), int(has_next_call)),
+           "aug_request_arrive")
+    return rec[0]
+
+
+def aug_request_return(rec: np.ndarray, realised: int, context_tokens: int, ret_tokens: int,
+                       pred_out: int, pred_call: float, has_next_call: int) -> np.ndarray:
+    """The record after a paused request's external call returned (a new
+    REQUEST_DTYPE element; `rec` is not modified)."""
+    out = np.array([rec], REQUEST_DTYPE)
+    _check(lib().aug_request_return(out.ctypes.data, int(realised), int(context_tokens), int(ret_tokens),
+                                    int(pred_out), float(pred_call), int(has_next_call)),
+           "aug_request_return")
+    return out[0]

@@ -1,4 +1,5 @@
-// Token-budget batch former: Algorithm 1, steps (3)-(4), of the paper.
+// Token-budget batch former: Algorithm 1, steps (3)-(4), of the paper, and
+// the request records of steps (1)-(2) (arrival, return of an external call).
 //
 // Per candidate request (running, swapped and waiting queues) it builds the
 // space-time cost C_{i,k} (Eq. cost) from the request's segment inputs -
@@ -8,9 +9,10 @@
 // Waste (Appendix B), and ranks by theta = (1 + beta w) / C (Eqs. value,
 // theta). The token budget is floor((G_free + G_preempt) / mu), clipped
 // (Eq. token). Packing walks the ranking and stops at the first request whose
-// tokens do not fit the budget or whose blocks cannot be found, reclaiming
-// blocks lazily from paused Swap (parked) and Discard (freed) requests. A
-// prefill request takes min(pending, chunk_cap, budget) tokens.
+// tokens do not fit the budget; a request whose blocks cannot be found is
+// passed over. Blocks are reclaimed lazily from paused Swap (parked) and
+// Discard (freed) requests. A prefill request takes min(pending, chunk_cap,
+// budget) tokens.
 //
 // Memory occupancy is counted in KV tokens after each iteration's tokens are
 // added, one iteration lasting t_iter seconds; mu is one token, so a budget
@@ -120,7 +122,7 @@ extern "C" aug_status aug_form_batch(const aug_request* reqs, int32_t n, int64_t
     return aug::fail(AUG_ERR_INVALID, "aug_form_batch: NULL argument or negative count");
   const aug_former_params& p = *params;
   if (!(p.t_iter > 0.0) || p.chunk_cap < 1 || p.block_size < 1 || p.t_max < 0 ||
-      free_blocks < 0 || out->cap < 0)
+      free_blocks < 0 || out->cap < 0 || p.order < AUG_ORDER_THETA || p.order > AUG_ORDER_SSJF)
     return aug::fail(AUG_ERR_INVALID, "aug_form_batch: bad parameters");
   if (out->cap > 0 && (!out->ids || !out->q_len || !out->theta || !out->resume_ids ||
                        !out->park_ids || !out->free_ids))
@@ -176,7 +178,9 @@ extern "C" aug_status aug_form_batch(const aug_request* reqs, int32_t n, int64_t
     return reqs[a].id < reqs[b].id;
   });
   std::sort(cand.begin(), cand.end(), [&](int32_t a, int32_t b) {
-    if (theta[a] != theta[b]) return theta[a] > theta[b];
+    if (p.order == AUG_ORDER_THETA && theta[a] != theta[b]) return theta[a] > theta[b];
+    if (p.order == AUG_ORDER_SSJF && reqs[a].pred_out != reqs[b].pred_out)
+      return reqs[a].pred_out < reqs[b].pred_out;
     if (reqs[a].arrival != reqs[b].arrival) return reqs[a].arrival < reqs[b].arrival;
     return reqs[a].id < reqs[b].id;
   });
@@ -196,10 +200,9 @@ extern "C" aug_status aug_form_batch(const aug_request* reqs, int32_t n, int64_t
     }
     const int64_t have = r.state == AUG_SWAPPED ? 0 : r.blocks_on_gpu;
     const int64_t need = std::max<int64_t>(0, (r.ctx_len + t + bs - 1) / bs - have);
-    if (need > free_now + reclaim_left) {
-      if (p.skip_instead_of_break) continue;
-      break;
-    }
+    // no memory for it now: passed over (the algorithm stops at the token
+    // budget only; memory enters through the budget)
+    if (need > free_now + reclaim_left) continue;
     while (need > free_now) {
       const aug_request& v = reqs[victims[vi++]];
       free_now += v.blocks_on_gpu;
@@ -229,5 +232,71 @@ extern "C" aug_status aug_form_batch(const aug_request* reqs, int32_t n, int64_t
   out->n_resume = n_resume;
   out->n_park = n_park;
   out->n_free = n_free;
+  return AUG_OK;
+}
+
+namespace {
+
+bool prediction_ok(int32_t pred_out, double pred_call) {
+  return pred_out >= 1 && std::isfinite(pred_call) && pred_call >= 0.0;
+}
+
+}  // namespace
+
+extern "C" aug_status aug_request_arrive(aug_request* r, int64_t id, double arrival, int32_t prompt_tokens,
+                                         int32_t pred_out, double pred_call, int32_t has_next_call) {
+  if (!r || prompt_tokens < 1 || !prediction_ok(pred_out, pred_call) || !std::isfinite(arrival))
+    return aug::fail(AUG_ERR_INVALID, "aug_request_arrive: NULL record or bad prompt/prediction");
+  aug_request q{};
+  q.id = id;
+  q.arrival = arrival;
+  q.last_sched = -1.0;
+  q.pred_call = has_next_call ? pred_call : 0.0;
+  q.pause_start = 0.0;
+  q.state = AUG_WAITING;
+  q.seg = 1;
+  q.prev_policy = AUG_POL_NONE;
+  q.cur_policy = AUG_POL_NONE;
+  q.seg_ctx = 0;
+  q.seg_prefill = prompt_tokens;
+  q.pred_out = pred_out;
+  q.has_next_call = has_next_call ? 1 : 0;
+  q.ctx_len = 0;
+  q.pending = prompt_tokens;
+  q.blocks_on_gpu = 0;
+  *r = q;
+  return AUG_OK;
+}
+
+extern "C" aug_status aug_request_return(aug_request* r, int32_t realised, int32_t context_tokens,
+                                         int32_t ret_tokens, int32_t pred_out, double pred_call,
+                                         int32_t has_next_call) {
+  if (!r) return aug::fail(AUG_ERR_INVALID, "aug_request_return: NULL record");
+  if (r->state != AUG_PAUSED)
+    return aug::fail(AUG_ERR_INVALID, "aug_request_return: request %lld is not paused", (long long)r->id);
+  if (realised != AUG_PRESERVE && realised != AUG_SWAP && realised != AUG_DISCARD)
+    return aug::fail(AUG_ERR_INVALID, "aug_request_return: unknown realised policy %d", realised);
+  if (context_tokens < r->ctx_len || ret_tokens < 0 || !prediction_ok(pred_out, pred_call))
+    return aug::fail(AUG_ERR_INVALID, "aug_request_return: bad context, return length or prediction");
+  r->seg += 1;
+  r->prev_policy = realised;
+  r->cur_policy = AUG_POL_NONE;
+  r->seg_ctx = context_tokens;
+  r->seg_prefill = ret_tokens;
+  r->pred_out = pred_out;
+  r->pred_call = has_next_call ? pred_call : 0.0;
+  r->has_next_call = has_next_call ? 1 : 0;
+  if (realised == AUG_PRESERVE) {
+    r->state = AUG_RUNNING;
+    r->pending = ret_tokens;
+  } else if (realised == AUG_SWAP) {
+    r->state = AUG_SWAPPED;
+    r->pending = ret_tokens;
+  } else {
+    r->state = AUG_WAITING;
+    r->ctx_len = 0;
+    r->blocks_on_gpu = 0;
+    r->pending = context_tokens + ret_tokens;
+  }
   return AUG_OK;
 }

@@ -133,3 +133,34 @@ def serving_former(**params):
                 arr[k] = [r[k] for r in recs]
         return aug_form_batch(arr, free_blocks, now, p)
     return run
+
+
+class _LibraryLifecycle:
+    """Request records of a serving loop, created and renewed by the library
+    (Algorithm 1, steps (1)-(2)). Records are dicts with the field names of
+    the library's request record."""
+
+    def __init__(self):
+        from . import REQUEST_DTYPE
+        self.dtype = REQUEST_DTYPE
+        self.names = [k for k in REQUEST_DTYPE.names if k != "reserved"]
+
+    def _dict(self, rec):
+        return {k: rec[k].item() for k in self.names}
+
+    def arrive(self, id, arrival, prompt_tokens, pred_out, pred_call, has_next_call):
+        from . import aug_request_arrive
+        return self._dict(aug_request_arrive(id, arrival, prompt_tokens, pred_out, pred_call, has_next_call))
+
+    def on_return(self, rec, realised, context_tokens, ret_tokens, pred_out, pred_call, has_next_call):
+        from . import aug_request_return
+        arr = np.zeros(1, self.dtype)
+        for k in self.names:
+            arr[0][k] = rec[k]
+        return self._dict(aug_request_return(arr[0], realised, context_tokens, ret_tokens, pred_out,
+                                             pred_call, has_next_call))
+
+
+def serving_lifecycle():
+    """The library's request-record transitions for ``synth.trace.ServingLoop``."""
+    return _LibraryLifecycle()

@@ -36,8 +36,8 @@ FORMER_PARAMS = dict(beta=5e-5, chunk_cap=512, t_iter=0.02, fwd_a=0.0175, fwd_b=
                      swap_s_per_tok=4.1e-8, n_fwd_max=1)
 
 
-def former_params(budget: int, dynamic: bool = True) -> dict:
-    p = dict(FORMER_PARAMS, t_max=int(budget))
+def former_params(budget: int, dynamic: bool = True, order: int = 0) -> dict:
+    p = dict(FORMER_PARAMS, t_max=int(budget), order=int(order))
     p.update(beta_low=0.5, beta_high=2.0) if dynamic else p.update(beta_low=1.0, beta_high=1.0)
     return p
 
@@ -50,13 +50,17 @@ class SweepRun:
     complete: bool                   # every request of the trace finished
     finished: int                    # requests that finished
     sim_seconds: float
+    metrics: dict                    # request-level results (ServingLoop.metrics)
 
 
-def run_budget(budget: int, former: Callable, seed: int = 0, dynamic: bool = True,
-               max_steps: int = 40_000, n_requests: int = 2000) -> SweepRun:
-    """Serve the seeded trace with ``former`` (built for this budget)."""
-    trace = make_trace(n=n_requests, seed=seed, rate=3.0)
-    loop = ServingLoop(trace, SimConfig(num_blocks=POOL_BLOCKS, max_preemptions=200))
+def run_budget(budget: int, former: Callable, lifecycle, seed: int = 0, dynamic: bool = True,
+               max_steps: int = 40_000, n_requests: int = 2000, rate: float = 3.0,
+               max_preemptions: int = 200) -> SweepRun:
+    """Serve the seeded trace (``rate`` arrivals per second) with ``former``
+    (built for this budget) and the request-record ``lifecycle`` (arrival and
+    call return)."""
+    trace = make_trace(n=n_requests, seed=seed, rate=rate)
+    loop = ServingLoop(trace, SimConfig(num_blocks=POOL_BLOCKS, max_preemptions=max_preemptions), lifecycle)
     try:
         loop.run(former, max_steps=max_steps)
     except RuntimeError as e:          # thrashing: the budget cannot serve the trace
@@ -65,7 +69,7 @@ def run_budget(budget: int, former: Callable, seed: int = 0, dynamic: bool = Tru
     steps = [s for s in loop.steps if s.ids]
     return SweepRun(budget=budget, dynamic=dynamic, steps=steps,
                     complete=len(loop.done) == n_requests, finished=len(loop.done),
-                    sim_seconds=loop.now)
+                    sim_seconds=loop.now, metrics=dict(loop.metrics(), preemptions=loop.preemptions))
 
 
 def prefill_pairs(step: StepRecord) -> int:

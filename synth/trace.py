@@ -9,15 +9,18 @@ true values times (1 + e) with e = +-p chosen at random, output lengths
 rounded up to 50-token buckets (the noise model and bucket size the paper
 uses for its predictor).
 
-The loop keeps every request in the scheduler's record format and, each
-iteration, asks a batch former (any callable) for a plan, then applies it:
+The loop keeps every request in the scheduler's record format. Records are
+created on arrival and renewed when a call returns by a ``lifecycle`` object
+(``arrive`` and ``on_return``: Algorithm 1, steps (1)-(2), normally the
+library's). Each iteration the loop asks a batch former (any callable) for a
+plan, then applies it:
 evictions (park or free), resumes, the chunk or decode token of every
 scheduled request, pauses, call returns with the policy that was actually
 realised (Swap if the context was parked, Discard if it was freed, Preserve
 if it stayed), completions, and a simulated clock. It contains none of the
 scheduler's arithmetic: budget, cost, priority, policy choice and packing all
-come from the former, so the oracle former and the C++ former can be driven in
-lock step. Iteration time follows a simple linear model of a large model on
+come from the former and the record transitions from the lifecycle, so the
+oracle and the C++ library can be driven in lock step. Iteration time follows a simple linear model of a large model on
 one GPU: t = t0 + a * (query tokens) + b * (context tokens).
 """
 
@@ -118,7 +121,8 @@ class ServingLoop:
     receives a list of dicts with the FIELDS keys and returns a dict with
     budget, ids, q_len, resume_ids, park_ids, free_ids and policy (per record)."""
 
-    def __init__(self, trace: List[TraceRequest], cfg: SimConfig = SimConfig()):
+    def __init__(self, trace: List[TraceRequest], cfg: SimConfig, lifecycle):
+        self.lifecycle = lifecycle
         self.trace = sorted(trace, key=lambda t: (t.arrival, t.id))
         self.cfg = cfg
         self.now = 0.0
@@ -148,28 +152,22 @@ class ServingLoop:
         return pred_out, pred_call, int(has_call)
 
     def _arrive(self, tr: TraceRequest):
-        lv = _Live(rec={f: 0 for f in FIELDS}, tr=tr)
+        lv = _Live(rec={}, tr=tr)
         pred_out, pred_call, has_call = self._predictions(lv)
-        lv.rec.update(id=tr.id, arrival=tr.arrival, last_sched=-1.0, state=WAITING, seg=1,
-                      prev_policy=NONE, cur_policy=NONE, seg_ctx=0, seg_prefill=tr.prompt,
-                      pred_out=pred_out, pred_call=pred_call, has_next_call=has_call, ctx_len=0,
-                      pending=tr.prompt, blocks_on_gpu=0, pause_start=0.0)
+        lv.rec = self.lifecycle.arrive(id=tr.id, arrival=tr.arrival, prompt_tokens=tr.prompt,
+                                       pred_out=pred_out, pred_call=pred_call, has_next_call=has_call)
         self.live[tr.id] = lv
 
     def _return(self, lv: _Live):
-        r = lv.rec
+        # the policy actually realised during the wait: Swap if the context was
+        # parked, Discard if it was freed, Preserve if it stayed
         realised = SWAP if lv.parked else DISCARD if lv.freed else PRESERVE
         ret = lv.tr.ret[lv.seg_index]
         lv.seg_index += 1
         pred_out, pred_call, has_call = self._predictions(lv)
-        r.update(seg=r["seg"] + 1, prev_policy=realised, cur_policy=NONE, seg_ctx=lv.logical_ctx,
-                 seg_prefill=ret, pred_out=pred_out, pred_call=pred_call, has_next_call=has_call)
-        if realised == PRESERVE:
-            r.update(state=RUNNING, pending=ret)
-        elif realised == SWAP:
-            r.update(state=SWAPPED, pending=ret)
-        else:
-            r.update(state=WAITING, ctx_len=0, pending=lv.logical_ctx + ret)
+        lv.rec = self.lifecycle.on_return(lv.rec, realised=realised, context_tokens=lv.logical_ctx,
+                                          ret_tokens=ret, pred_out=pred_out, pred_call=pred_call,
+                                          has_next_call=has_call)
         lv.parked = lv.freed = False
 
     # ---- one iteration -------------------------------------------------------------
@@ -298,6 +296,28 @@ class ServingLoop:
             self.last_ids = set(ids)
         self.steps.append(rec)
         return rec
+
+    def metrics(self, slo_ttft: float = 1.0, slo_norm: Optional[float] = None) -> dict:
+        """Request-level results of the finished requests: time to first token
+        (queueing included), normalized latency (end-to-end latency over output
+        tokens) and goodput (requests per second meeting both SLOs, over the
+        time from the first arrival to the last completion). The default
+        normalized-latency SLO is ten times the model's base iteration time."""
+        if slo_norm is None:
+            slo_norm = 10.0 * self.cfg.t0
+        ids = sorted(self.done)
+        if not ids:
+            return dict(finished=0, ttft_mean=None, ttft_p50=None, ttft_p99=None, norm_latency_mean=None,
+                        goodput=0.0, slo_ttft=slo_ttft, slo_norm=slo_norm)
+        out_len = {t.id: t.output for t in self.trace}
+        ttft = np.array([self.done[i][1] - self.done[i][0] for i in ids])
+        norm = np.array([(self.done[i][2] - self.done[i][0]) / max(1, out_len[i]) for i in ids])
+        span = max(self.done[i][2] for i in ids) - min(self.done[i][0] for i in ids)
+        good = int(np.count_nonzero((ttft < slo_ttft) & (norm < slo_norm)))
+        return dict(finished=len(ids), ttft_mean=float(ttft.mean()), ttft_p50=float(np.median(ttft)),
+                    ttft_p99=float(np.percentile(ttft, 99)), norm_latency_mean=float(norm.mean()),
+                    goodput=good / span if span > 0 else 0.0, slo_met=good, slo_ttft=slo_ttft,
+                    slo_norm=slo_norm)
 
     def run(self, former: Callable, max_steps: Optional[int] = None) -> List[StepRecord]:
         n = 0

@@ -1,6 +1,8 @@
 """Former callables for the serving loop: the oracle (pure Python) and the
 C++ library, both returning the same plan dict."""
 
+import dataclasses
+
 import numpy as np
 
 from oracle import former as of
@@ -21,7 +23,7 @@ def library_former(params: of.Params, block_size: int = 16):
                            beta_high=params.beta_high, chunk_cap=params.chunk_cap, t_iter=params.t_iter,
                            fwd_a=params.fwd_a, fwd_b=params.fwd_b, swap_s_per_tok=params.swap_s_per_tok,
                            n_fwd_max=params.n_fwd_max, skip_instead_of_break=params.skip_instead_of_break,
-                           block_size=block_size)
+                           block_size=block_size, order=params.order)
 
     def run(recs, free_blocks, now):
         arr = np.zeros(len(recs), aug.REQUEST_DTYPE)
@@ -46,3 +48,40 @@ def lockstep(oracle, library):
             assert list(a[k]) == list(b[k]), k
         return b
     return run
+
+
+class OracleLifecycle:
+    """Request-record transitions of the oracle (Algorithm 1, steps (1)-(2))."""
+
+    def arrive(self, **kw):
+        return dataclasses.asdict(of.arrive(**kw))
+
+    def on_return(self, rec, **kw):
+        return dataclasses.asdict(of.on_return(of.Request(**rec), **kw))
+
+
+class LockstepLifecycle:
+    """Both lifecycles on every event; records must agree bit for bit."""
+
+    def __init__(self):
+        import paper_2512_04013_amd.runtime as rt
+        self.a, self.b = OracleLifecycle(), rt.serving_lifecycle()
+
+    @staticmethod
+    def _same(x, y):
+        assert set(x) == set(y)
+        for k in x:
+            if isinstance(x[k], float) or isinstance(y[k], float):
+                assert np.float64(x[k]).view(np.uint64) == np.float64(y[k]).view(np.uint64), k
+            else:
+                assert x[k] == y[k], (k, x[k], y[k])
+
+    def arrive(self, **kw):
+        x, y = self.a.arrive(**kw), self.b.arrive(**kw)
+        self._same(x, y)
+        return y
+
+    def on_return(self, rec, **kw):
+        x, y = self.a.on_return(dict(rec), **kw), self.b.on_return(dict(rec), **kw)
+        self._same(x, y)
+        return y

@@ -31,7 +31,7 @@ def formed_batches():
     from paper_2512_04013_amd import runtime as rt
     seen, cases = set(), []
     for budget in sweep.BUDGETS:
-        run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)),
+        run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), rt.serving_lifecycle(),
                                max_steps=MAX_STEPS.get(budget, 40_000))
         say(f"[sweep] budget {budget}: {len(run.steps)} batches, complete={run.complete}")
         picks = sweep.select_steps(run.steps, 1, seed=budget)

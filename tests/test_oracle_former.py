@@ -150,6 +150,27 @@ def test_equal_cost_longest_waiting_first():
     assert of.form_batch(reqs, 10**6, 16, 1.0, p).ids == [3, 5, 7]
 
 
+def test_fcfs_ranks_by_arrival_whatever_the_cost():
+    rng = np.random.default_rng(3)
+    reqs = [_running(i, int(rng.integers(10, 2000)), int(rng.integers(1, 300)),
+                     arrival=float(rng.uniform(0, 5)), last=float(rng.uniform(5, 6))) for i in range(30)]
+    p = Params(t_max=10_000, beta_low=1, beta_high=1, order=of.ORDER_FCFS)
+    plan = of.form_batch(reqs, free_blocks=10**6, block_size=16, now=10.0, p=p)
+    assert plan.ids == [r.id for r in sorted(reqs, key=lambda r: r.arrival)]
+    # theta order differs on the same requests, so the key really changed
+    theta_plan = of.form_batch(reqs, 10**6, 16, 10.0, Params(t_max=10_000, beta_low=1, beta_high=1))
+    assert theta_plan.ids != plan.ids and sorted(theta_plan.ids) == sorted(plan.ids)
+
+
+def test_ssjf_ranks_by_predicted_output_then_arrival():
+    outs = [300, 50, 50, 1000, 2, 50]
+    reqs = [_running(i, 100 + 37 * i, o, arrival=float(5 - i)) for i, o in enumerate(outs)]
+    p = Params(t_max=10_000, beta_low=1, beta_high=1, order=of.ORDER_SSJF)
+    plan = of.form_batch(reqs, free_blocks=10**6, block_size=16, now=10.0, p=p)
+    # pred_out 2, then the three 50s by arrival (ids 5, 2, 1 arrived at 0, 3, 4), then 300, 1000
+    assert plan.ids == [4, 5, 2, 1, 0, 3]
+
+
 # ---- packing ---------------------------------------------------------------------------
 
 def _mixed_2048_requests(extra_decode=False):

@@ -10,7 +10,7 @@ import paper_2512_04013_amd as aug
 from oracle import former as of
 from synth import sweep
 from synth.trace import PAUSED, ServingLoop, SimConfig, make_trace
-from tests.former_drivers import library_former, lockstep, oracle_former
+from tests.former_drivers import LockstepLifecycle, OracleLifecycle, library_former, lockstep, oracle_former
 
 pytestmark = pytest.mark.skipif(not os.path.exists(aug.LIB_PATH), reason="libaug.so not built")
 
@@ -40,7 +40,7 @@ def test_trace_is_seeded_and_shaped():
 def test_loop_runs_both_formers_in_lock_step(budget, dynamic, blocks):
     trace = small_trace(seed=budget)
     p = params_for(budget, dynamic)
-    loop = ServingLoop(trace, SimConfig(num_blocks=blocks))
+    loop = ServingLoop(trace, SimConfig(num_blocks=blocks), LockstepLifecycle())
     steps = loop.run(lockstep(oracle_former(p), library_former(p)))
     assert len(loop.done) == len(trace)
     assert all(sum(s.q_len) <= s.budget for s in steps)
@@ -57,7 +57,7 @@ def test_paused_requests_are_never_scheduled():
     trace = small_trace(seed=9)
     p = params_for(1024, True)
     lib = library_former(p)
-    loop = ServingLoop(trace, SimConfig(num_blocks=384))
+    loop = ServingLoop(trace, SimConfig(num_blocks=384), OracleLifecycle())
 
     def checked(recs, free, now):
         plan = lib(recs, free, now)
@@ -71,7 +71,7 @@ def test_paused_requests_are_never_scheduled():
 
 def test_a_pool_far_too_small_is_reported_not_looped_on():
     trace = small_trace(seed=256)
-    loop = ServingLoop(trace, SimConfig(num_blocks=256, max_preemptions=200))
+    loop = ServingLoop(trace, SimConfig(num_blocks=48, max_preemptions=200), OracleLifecycle())
     with pytest.raises(RuntimeError, match="thrashing"):
         loop.run(library_former(params_for(256, False)))
 
@@ -83,7 +83,7 @@ def test_lock_step_on_a_prefix_of_the_full_size_trace(budget):
     too long for the pure-Python former in the CPU suite)."""
     trace = make_trace(n=2000, seed=1, rate=3.0)
     p = params_for(budget, True)
-    loop = ServingLoop(trace, SimConfig(num_blocks=16384))
+    loop = ServingLoop(trace, SimConfig(num_blocks=16384), LockstepLifecycle())
     steps = loop.run(lockstep(oracle_former(p), library_former(p)), max_steps=400)
     assert len(steps) == 400
     assert all(sum(s.q_len) <= s.budget for s in steps)
@@ -105,7 +105,7 @@ def test_serving_former_marshals_like_the_test_driver():
         assert np.array_equal(np.asarray(a["theta"]).view(np.uint64), np.asarray(b["theta"]).view(np.uint64))
         return a
 
-    loop = ServingLoop(make_trace(n=2000, seed=2), SimConfig(num_blocks=16384))
+    loop = ServingLoop(make_trace(n=2000, seed=2), SimConfig(num_blocks=16384), rt.serving_lifecycle())
     assert len(loop.run(both, max_steps=300)) == 300
 
 
@@ -113,8 +113,48 @@ def test_sweep_budgets_from_512_serve_the_whole_trace():
     """Every request of the 2000-request trace finishes under budget 512 with
     the 16,384-block pool; budget 256 overloads it (the loop stops early)."""
     from paper_2512_04013_amd import runtime as rt
-    run = sweep.run_budget(512, rt.serving_former(**sweep.former_params(512)))
+    run = sweep.run_budget(512, rt.serving_former(**sweep.former_params(512)), rt.serving_lifecycle())
     assert run.complete and run.finished == 2000
     assert all(sum(s.q_len) <= s.budget for s in run.steps)
-    small = sweep.run_budget(256, rt.serving_former(**sweep.former_params(256)), max_steps=2000)
+    small = sweep.run_budget(256, rt.serving_former(**sweep.former_params(256)), rt.serving_lifecycle(),
+                             max_steps=2000)
     assert not small.complete
+
+
+@pytest.mark.parametrize("order", [of.ORDER_FCFS, of.ORDER_SSJF])
+def test_baseline_orders_run_both_formers_in_lock_step(order):
+    trace = small_trace(seed=30 + order)
+    p = of.Params(**sweep.former_params(1024, True, order=order))
+    loop = ServingLoop(trace, SimConfig(num_blocks=384), LockstepLifecycle())
+    steps = loop.run(lockstep(oracle_former(p), library_former(p)))
+    assert len(loop.done) == len(trace)
+    assert all(sum(s.q_len) <= s.budget for s in steps)
+
+
+def test_request_records_match_the_oracle_on_every_transition_kind():
+    """Arrival, and a return under each realised policy, through the library
+    and the oracle, compared field by field."""
+    lc = LockstepLifecycle()
+    rec = lc.arrive(id=7, arrival=2.5, prompt_tokens=300, pred_out=150, pred_call=0.4, has_next_call=1)
+    assert rec["state"] == of.WAITING and rec["pending"] == 300 and rec["seg"] == 1
+    for realised, state in ((of.PRESERVE, of.RUNNING), (of.SWAP, of.SWAPPED), (of.DISCARD, of.WAITING)):
+        paused = dict(rec, state=of.PAUSED, ctx_len=0 if realised == of.DISCARD else 460,
+                      blocks_on_gpu=0 if realised != of.PRESERVE else 29, cur_policy=realised)
+        out = lc.on_return(paused, realised=realised, context_tokens=460, ret_tokens=90, pred_out=50,
+                           pred_call=0.0, has_next_call=0)
+        assert out["state"] == state and out["seg"] == 2 and out["prev_policy"] == realised
+        assert out["pending"] == (550 if realised == of.DISCARD else 90)
+        assert out["seg_ctx"] == 460 and out["seg_prefill"] == 90 and out["pred_call"] == 0.0
+
+
+def test_library_rejects_bad_record_transitions():
+    from paper_2512_04013_amd import REQUEST_DTYPE, AugError
+    with pytest.raises(AugError):
+        aug.aug_request_arrive(1, 0.0, 0, 10, 0.0, 0)            # empty prompt
+    rec = aug.aug_request_arrive(1, 0.0, 10, 10, 0.0, 0)
+    with pytest.raises(AugError):
+        aug.aug_request_return(rec, of.PRESERVE, 10, 5, 10, 0.0, 0)   # not paused
+    rec["state"] = of.PAUSED
+    with pytest.raises(AugError):
+        aug.aug_request_return(rec, 9, 10, 5, 10, 0.0, 0)              # unknown policy
+    assert REQUEST_DTYPE.itemsize > 0
