@@ -44,6 +44,8 @@ WORKLOADS = {
     # under an 8192-token budget, on the 64/8-head fp8-KV layer
     "sweep-prefill-fp8": 5,   # the batch with the most prefill query-key pairs
     "sweep-context-fp8": 5,   # the batch with the most context tokens
+    # 512 decodes on the same 64/8-head fp8 layer (decode-dominated, full size)
+    "decode-fp8-64x8": 7,
     # every budget 256 ... 8192: a sample of the formed batches replayed on one pool
     "budget-sweep-fp8": 6,
 }
@@ -202,6 +204,8 @@ def make_workload(name: str, seed: int, log):
     """The workload's batch and the budget T_max it is formed under."""
     import synth
     cfg = WORKLOADS[name]
+    if cfg == 7:
+        return synth.make_decode_gqa8_fp8(seed=seed), 8192
     if cfg != 5:
         return synth.make_config(cfg, seed=seed), 2048
     from synth import sweep

@@ -68,6 +68,11 @@ constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running max
 // denominator always share one reference, so the result is unchanged.
 constexpr float kRescaleSlack = 8.0f;
 constexpr int kThreads = 256;
+#ifndef AUG_ROW_MFMA
+#define AUG_ROW_MFMA 1
+#endif
+constexpr bool kRowMfma = AUG_ROW_MFMA;   // 8-way GQA decode rows on MFMA
+
 
 enum : int { KV_F32 = 0, KV_BF16 = 1, KV_FP8 = 2 };
 
@@ -103,6 +108,9 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
 }
 
 typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+constexpr uint32_t kBf16PairOne = 0x3F803F80u;   // (1.0, 1.0) as packed bf16
 
 // two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32)
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
@@ -357,6 +365,49 @@ __device__ __forceinline__ void finish_split(const AttnArgs& a, int group, int n
 // row items (VALU)
 // ---------------------------------------------------------------------------
 
+// Last step of a row item: every wave has written its unnormalised output
+// o[G][D], running maximum and row sum to lds[wave][head][D + 2]; the waves'
+// results are merged (log-sum-exp) and stored as the output rows, or as the
+// item's split-K partial.
+template <int D, int G, int OT>
+__device__ __forceinline__ void row_merge_waves(const WorkItem& it, const AttnArgs& a, float* lds) {
+  constexpr int ROW = D + 2;
+  const int kvh = it.kvh;
+  __syncthreads();
+  constexpr int NW = kThreads / 64;
+  for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
+    const int h = idx / D;
+    const int d = idx % D;
+    float mw[NW];
+    float mx = kNegBig;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      mw[w] = lds[(w * G + h) * ROW + D];
+      mx = fmaxf(mx, mw[w]);
+    }
+    float ls = 0.f, os = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float f = __builtin_amdgcn_exp2f(mw[w] - mx);
+      ls += lds[(w * G + h) * ROW + D + 1] * f;
+      os += lds[(w * G + h) * ROW + d] * f;
+    }
+    if (it.part < 0) {
+      const int64_t off = (static_cast<int64_t>(it.q_row0) * a.hq + static_cast<int64_t>(kvh) * G + h) * D + d;
+      store_out<OT>(a.out, off, os / ls);
+    } else {
+      float* pp = a.partials + static_cast<int64_t>(it.part) * aug::partial_floats(G, D);
+      store_partial(pp + h * D + d, os);
+      if (d == 0) {
+        store_partial(pp + G * D + h, mx);
+        store_partial(pp + G * D + G + h, ls);
+      }
+    }
+  }
+  if (it.part >= 0) finish_split<D, G, OT, kThreads>(a, it.group, 1, lds);
+}
+
+
 template <int KVT, int D, int G, int QT, int OT, bool PREFETCH>
 __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   using F = KvFmt<KVT>;
@@ -548,38 +599,265 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
       }
     }
   }
-  __syncthreads();
-  constexpr int NW = kThreads / 64;
-  for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
-    const int h = idx / D;
-    const int d = idx % D;
-    float mw[NW];
-    float mx = kNegBig;
+  row_merge_waves<D, G, OT>(it, a, lds);
+}
+
+// ---------------------------------------------------------------------------
+// row items of 8-way grouped-query attention (MFMA)
+// ---------------------------------------------------------------------------
+//
+// With eight query heads per KV head, a decode row's work per KV byte (two
+// bf16 dot products of D per head and key) is more than the vector ALUs keep
+// up with next to fp8 decoding, so the eight heads go through 16x16 bf16
+// MFMAs instead (heads 8..15 of each MFMA are zero padding). Per 16-token
+// block and wave:
+//   S^T[16 keys][16 heads] = K Q^T with four 16x16x32 MFMAs over head_dim.
+//     Lane l holds token l % 16 and dims 32g .. 32g + 31 (g = l / 16) of the
+//     block's K rows; k-step s takes dims 32g + 8s .. + 8 of both K and Q (a
+//     permutation of the reduction dimension shared by both operands).
+//   The S^T accumulator gives lane l head l % 16 and keys 4g .. 4g + 3, which
+//   is exactly the B operand layout of a 16x16x16 MFMA over those keys, so
+//   the probabilities feed PV without any exchange.
+//   O^T[128 dims][16 heads] += V^T P^T with eight 16x16x16 MFMAs, one per dim
+//     block b: row m of block b is dim 8m + b, so lane l loads dims 8m .. 8m + 7
+//     (m = l % 16) of its four tokens 4g .. 4g + 3 with contiguous loads and
+//     only regroups them into (token, token) pairs per dim.
+// The resulting accumulators give lane l head l % 16 and dims 32g .. 32g + 31.
+
+// max and sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48
+__device__ __forceinline__ float group4_max(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  const float m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float group4_sum(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  const float m = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+// OCP E4M3FN byte pair (bytes 0-1, or 2-3 with HI) -> exact bf16 pair
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+}
+
+template <int KVT> struct MfmaRowKv;
+template <> struct MfmaRowKv<KV_BF16> {
+  struct K { uint4 w[4]; };      // token l % 16, dims 32g .. 32g + 31
+  struct V { uint4 w[4]; };      // tokens 4g + t, dims 8m .. 8m + 7
+  static constexpr int EB = 2;
+  __device__ static void load_k(const char* p, K& k) {
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      mw[w] = lds[(w * G + h) * ROW + D];
-      mx = fmaxf(mx, mw[w]);
-    }
-    float ls = 0.f, os = 0.f;
+    for (int i = 0; i < 4; ++i) k.w[i] = reinterpret_cast<const uint4*>(p)[i];
+  }
+  __device__ static void load_v(const char* p, int64_t row_bytes, V& v) {
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float f = __builtin_amdgcn_exp2f(mw[w] - mx);
-      ls += lds[(w * G + h) * ROW + D + 1] * f;
-      os += lds[(w * G + h) * ROW + d] * f;
-    }
-    if (it.part < 0) {
-      const int64_t off = (static_cast<int64_t>(it.q_row0) * a.hq + static_cast<int64_t>(kvh) * G + h) * D + d;
-      store_out<OT>(a.out, off, os / ls);
-    } else {
-      float* pp = a.partials + static_cast<int64_t>(it.part) * aug::partial_floats(G, D);
-      store_partial(pp + h * D + d, os);
-      if (d == 0) {
-        store_partial(pp + G * D + h, mx);
-        store_partial(pp + G * D + G + h, ls);
-      }
+    for (int t = 0; t < 4; ++t) v.w[t] = *reinterpret_cast<const uint4*>(p + t * row_bytes);
+  }
+  __device__ static uint4 k_operand(const K& k, int s) { return k.w[s]; }
+  __device__ static void zero_v(V& v, int t) { v.w[t] = uint4{0, 0, 0, 0}; }
+  // (token 4g + 0..3) values of dim 8m + b, as two bf16 pairs
+  __device__ static void v_operands(const V& v, uint2 (&op)[8]) {
+    const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&v.w[0]);
+    const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&v.w[1]);
+    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&v.w[2]);
+    const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&v.w[3]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      op[2 * i] = uint2{__builtin_amdgcn_perm(x1[i], x0[i], 0x05040100u), __builtin_amdgcn_perm(x3[i], x2[i], 0x05040100u)};
+      op[2 * i + 1] = uint2{__builtin_amdgcn_perm(x1[i], x0[i], 0x07060302u), __builtin_amdgcn_perm(x3[i], x2[i], 0x07060302u)};
     }
   }
-  if (it.part >= 0) finish_split<D, G, OT, kThreads>(a, it.group, 1, lds);
+};
+template <> struct MfmaRowKv<KV_FP8> {
+  struct K { uint4 w[2]; };
+  struct V { uint2 w[4]; };
+  static constexpr int EB = 1;
+  __device__ static void load_k(const char* p, K& k) {
+    k.w[0] = reinterpret_cast<const uint4*>(p)[0];
+    k.w[1] = reinterpret_cast<const uint4*>(p)[1];
+  }
+  __device__ static void load_v(const char* p, int64_t row_bytes, V& v) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) v.w[t] = *reinterpret_cast<const uint2*>(p + t * row_bytes);
+  }
+  __device__ static uint4 k_operand(const K& k, int s) {
+    const uint4& w = k.w[s >> 1];
+    const uint32_t lo = (s & 1) ? w.z : w.x, hi = (s & 1) ? w.w : w.y;
+    return uint4{fp8x2_to_bf16x2<false>(lo), fp8x2_to_bf16x2<true>(lo), fp8x2_to_bf16x2<false>(hi),
+                 fp8x2_to_bf16x2<true>(hi)};
+  }
+  __device__ static void zero_v(V& v, int t) { v.w[t] = uint2{0, 0}; }
+  __device__ static void v_operands(const V& v, uint2 (&op)[8]) {
+    // interleave the bytes of tokens (0, 1) and (2, 3), then each byte pair
+    // converts to the bf16 pair (token, token + 1) of one dim
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t a0 = i ? v.w[0].y : v.w[0].x, a1 = i ? v.w[1].y : v.w[1].x;
+      const uint32_t a2 = i ? v.w[2].y : v.w[2].x, a3 = i ? v.w[3].y : v.w[3].x;
+      const uint32_t p01lo = __builtin_amdgcn_perm(a1, a0, 0x05010400u);   // dims 4i, 4i+1
+      const uint32_t p01hi = __builtin_amdgcn_perm(a1, a0, 0x07030602u);   // dims 4i+2, 4i+3
+      const uint32_t p23lo = __builtin_amdgcn_perm(a3, a2, 0x05010400u);
+      const uint32_t p23hi = __builtin_amdgcn_perm(a3, a2, 0x07030602u);
+      op[4 * i + 0] = uint2{fp8x2_to_bf16x2<false>(p01lo), fp8x2_to_bf16x2<false>(p23lo)};
+      op[4 * i + 1] = uint2{fp8x2_to_bf16x2<true>(p01lo), fp8x2_to_bf16x2<true>(p23lo)};
+      op[4 * i + 2] = uint2{fp8x2_to_bf16x2<false>(p01hi), fp8x2_to_bf16x2<false>(p23hi)};
+      op[4 * i + 3] = uint2{fp8x2_to_bf16x2<true>(p01hi), fp8x2_to_bf16x2<true>(p23hi)};
+    }
+  }
+};
+
+template <int KVT, int OT>
+__device__ void row_item_mfma(const WorkItem& it, const AttnArgs& a, float* lds) {
+  constexpr int D = 128, G = 8;
+  constexpr bool FP8 = KVT == KV_FP8;
+  using KV = MfmaRowKv<KVT>;
+  constexpr int EB = KV::EB;
+  const int lane = threadIdx.x & 63;
+  // wave-uniform, so block ids and scales come through scalar loads instead
+  // of queueing behind the K/V loads
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int j = lane & 15;            // query head of the group (8..15: padding)
+  const int g = lane >> 4;            // keys 4g .. 4g + 3 of a block
+  const int kvh = it.kvh;
+
+  // Q^T operands of the four k-steps: dims 32g + 8s .. + 8 of head j
+  uint4 qop[4];
+  {
+    const uint16_t* qb = static_cast<const uint16_t*>(a.q) +
+                         (static_cast<int64_t>(it.q_row0) * a.hq + static_cast<int64_t>(kvh) * G + (j & 7)) * D + 32 * g;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qop[s] = j < G ? *reinterpret_cast<const uint4*>(qb + 8 * s) : uint4{0, 0, 0, 0};
+  }
+  const float sc = a.scale_log2;
+  float m_run = kNegBig, l_run = 0.f;
+  f32x4_t oacc[8];
+#pragma unroll
+  for (int b = 0; b < 8; ++b) oacc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int blk0 = it.key_begin / kBlock;
+  const int nblk = (it.key_end - it.key_begin + kBlock - 1) / kBlock;
+  constexpr int64_t kRow = static_cast<int64_t>(D) * EB;                 // bytes of one token row
+  constexpr int64_t kHead = kBlock * kRow;                               // bytes of one (block, head)
+  const char* kc = static_cast<const char*>(a.k_cache);
+  const char* vc = static_cast<const char*>(a.v_cache);
+  const int64_t k_lane = (j * D + 32 * g) * EB;                          // token j, dims 32g..
+  const int64_t v_lane = (4 * g * D + 8 * j) * EB;                       // tokens 4g.., dims 8j..
+  constexpr int kWaves = kThreads / 64;
+  const int32_t* table = a.block_ids + it.bt_off + blk0;
+  // a block's K and V, and (fp8) its two scales, loaded together so the
+  // scales arrive with the data instead of a memory round trip later
+  struct Scales { float k, v; };
+  auto load_block = [&](int bid, typename KV::K& k, typename KV::V& v, Scales& sc2) {
+    if (static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks)) {
+      const int64_t base = (static_cast<int64_t>(bid) * a.hkv + kvh) * kHead;
+      KV::load_k(kc + base + k_lane, k);
+      KV::load_v(vc + base + v_lane, kRow, v);
+      if constexpr (FP8) {
+        sc2.k = a.k_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
+        sc2.v = a.v_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
+      }
+    } else {
+      k = typename KV::K{};
+      v = typename KV::V{};
+      sc2 = Scales{1.f, 1.f};
+    }
+  };
+
+  // the next block's K/V (and scales) in flight while one is computed, its
+  // id read one iteration before that (deeper prefetch measured no faster)
+  typename KV::K kpre{};
+  typename KV::V vpre{};
+  Scales spre{1.f, 1.f};
+  int bid_pre = wave < nblk ? __builtin_amdgcn_readfirstlane(table[wave]) : 0;
+  if (wave < nblk) load_block(bid_pre, kpre, vpre, spre);
+  int bid_next = wave + kWaves < nblk ? table[wave + kWaves] : 0;
+  for (int bi = wave; bi < nblk; bi += kWaves) {
+    const int tok0 = (blk0 + bi) * kBlock;
+    const int bid = bid_pre;
+    typename KV::K kraw = kpre;
+    typename KV::V vraw = vpre;
+    const Scales bsc = spre;
+    if (bi + kWaves < nblk) {
+      bid_pre = __builtin_amdgcn_readfirstlane(bid_next);
+      load_block(bid_pre, kpre, vpre, spre);
+      if (bi + 2 * kWaves < nblk) bid_next = table[bi + 2 * kWaves];
+    }
+    const bool bid_ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
+    float ksc = sc, vlog = 0.f, vinv = 1.f;
+    if constexpr (FP8) {
+      if (bid_ok) {
+        ksc = sc * bsc.k;
+        // the V scale enters each probability through its log2 and leaves the
+        // row sum through its reciprocal (a zero scale is taken as 2^-100)
+        const float vs = fmaxf(bsc.v, 0x1p-100f);
+        vlog = __builtin_amdgcn_logf(vs);
+        vinv = __builtin_amdgcn_rcpf(vs);
+      }
+    }
+
+    f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(KV::k_operand(kraw, s)), as_bf16x8(qop[s]), sacc,
+                                                     0, 0, 0);
+    // a block is inside the span (no masking) or the span's tail / an unusable block
+    const bool full = bid_ok && tok0 + kBlock <= it.key_end;
+    float sv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sv[r] = sacc[r] * ksc;
+    if (!full) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool valid = bid_ok && tok0 + 4 * g + r < it.key_end;
+        sv[r] = valid ? sv[r] : -INFINITY;
+        if (!valid) KV::zero_v(vraw, r);   // zero, so 0 * value never meets NaN
+      }
+    }
+    const float bm = group4_max(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])));
+    const float mn = fmaxf(m_run, bm);
+    if (__any(mn > m_run + kRescaleSlack)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
+      l_run *= alpha;
+#pragma unroll
+      for (int b = 0; b < 8; ++b) oacc[b] *= alpha;
+      m_run = mn;
+    }
+    const float bias = vlog - m_run;
+    const uint32_t p01 = pack_bf16(__builtin_amdgcn_exp2f(sv[0] + bias), __builtin_amdgcn_exp2f(sv[1] + bias));
+    const uint32_t p23 = pack_bf16(__builtin_amdgcn_exp2f(sv[2] + bias), __builtin_amdgcn_exp2f(sv[3] + bias));
+    // the row sum adds exactly the packed probabilities
+    const float bsum = dot2_bf16(p23, kBf16PairOne, dot2_bf16(p01, kBf16PairOne, 0.f));
+    l_run = FP8 ? fmaf(bsum, vinv, l_run) : l_run + bsum;
+    const s16x4_t pop = __builtin_bit_cast(s16x4_t, uint2{p01, p23});
+    uint2 vop[8];
+    KV::v_operands(vraw, vop);
+#pragma unroll
+    for (int b = 0; b < 8; ++b)
+      oacc[b] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4_t, vop[b]), pop, oacc[b], 0, 0, 0);
+  }
+
+  // this wave's result for head j: dims 32g + 8r + b from oacc[b][r]
+  constexpr int ROW = D + 2;
+  const float l_tot = group4_sum(l_run);
+  if (j < G) {
+    float* dst = lds + (wave * G + j) * ROW;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int b = 0; b < 8; ++b) dst[32 * g + 8 * r + b] = oacc[b][r];
+    if (g == 0) {
+      dst[D] = m_run;
+      dst[D + 1] = l_tot;
+    }
+  }
+  row_merge_waves<D, G, OT>(it, a, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -621,7 +899,6 @@ template <> struct TileStage<KV_FP8> {
   }
 };
 
-__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef bf16x4_t __attribute__((address_space(3))) lds_bf16x4_t;
@@ -642,7 +919,6 @@ __device__ __forceinline__ float sum_across_halves(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-constexpr uint32_t kBf16PairOne = 0x3F803F80u;   // (1.0, 1.0) as packed bf16
 
 template <bool B> using bool_tag = std::integral_constant<bool, B>;
 
@@ -989,7 +1265,10 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   }
   // row items always fetch a wave's next block while the current one is
   // computed: short spans (small batches) are latency bound otherwise
-  row_item<KVT, D, G, QT, OT, true>(it, a, reinterpret_cast<float*>(smem));
+  if constexpr (kRowMfma && G == 8 && D == 128 && (KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16)
+    row_item_mfma<KVT, OT>(it, a, reinterpret_cast<float*>(smem));
+  else
+    row_item<KVT, D, G, QT, OT, true>(it, a, reinterpret_cast<float*>(smem));
 }
 
 // Batches without prefill tiles: row items only, sized for high occupancy.

@@ -438,6 +438,20 @@ def make_long_context(seed: int = 0, sharp: bool = False, n_req: int = 64, n_mov
         extra_reqs_ctx=parked_ctx, resume_mask=mask)
 
 
+def make_decode_gqa8_fp8(seed: int = 0, sharp: bool = False, n_req: int = 512) -> AttnBatch:
+    """A decode-only batch on the budget sweep's layer (64 query heads, 8 KV
+    heads, head_dim 128, bf16 Q, fp8 E4M3FN KV with per-block scales):
+    ``n_req`` decodes with contexts lognormal (median 2500, sigma 0.8, capped
+    at 16384), the decode-dominated end of the batches a large budget forms."""
+    rng = np.random.default_rng(seed)
+    ctx = np.clip(np.rint(rng.lognormal(np.log(2500.0), 0.8, n_req)), 1, 16384).astype(np.int64)
+    pool = int(((ctx + BLOCK - 1) // BLOCK).sum()) * 5 // 4 + 64
+    return make_batch_from_lengths(
+        "decode-fp8-64x8", [1] * n_req, ctx.tolist(), num_q_heads=64, num_kv_heads=8, head_dim=128,
+        q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16", n_pool_blocks=pool, seed=seed + 2000,
+        kv_std=1.0 if sharp else 1.0 / np.sqrt(128.0))
+
+
 def make_config(cfg: int, seed: int = 0, sharp: bool = False, **kw) -> AttnBatch:
     if cfg == 1:
         return make_tiny_mixed(seed, **kw)

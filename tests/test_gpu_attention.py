@@ -115,6 +115,28 @@ def test_decode_8b_full(decode_8b, split):
     compare(got, want, "bf16", what=f"decode-8b split={split} items={att.info.num_items}")
 
 
+@pytest.mark.parametrize("kv", ["fp8", "bf16"])
+@pytest.mark.parametrize("sharp", [False, True])
+def test_gqa8_decode_batch_full_size(kv, sharp):
+    """512 decodes on the 64/8-head layer (the shape of the budget sweep),
+    contexts lognormal (median 2500, sigma 0.8, cap 16384): the 8-way grouped
+    decode rows run on the MFMA row path. Every row of a sample of 64
+    requests (and the shortest and longest) against the oracle."""
+    rng = np.random.default_rng(21)
+    ctx = np.clip(np.rint(rng.lognormal(np.log(2500), 0.8, 512)), 1, 16384).astype(int)
+    b = make_batch_from_lengths("gqa8-decode", [1] * 512, ctx.tolist(), num_q_heads=64, num_kv_heads=8,
+                                head_dim=128, q_dtype="bf16", kv_dtype=kv, out_dtype="bf16",
+                                n_pool_blocks=int(sum(-(-c // 16) for c in ctx)) + 64, seed=22,
+                                kv_std=1.0 if sharp else 1.0 / np.sqrt(128.0))
+    say(f"[gqa8 decode] kv={kv} sharp={sharp} keys={int(ctx.sum())}")
+    got, att = _run(b)
+    reqs = sorted(set([int(np.argmin(ctx)), int(np.argmax(ctx))] +
+                      [int(r) for r in np.random.default_rng(23).choice(512, 64, replace=False)]))
+    want = oa.attention_for(b, requests=reqs)
+    compare(got, want, "bf16", rows=rows_of(b, reqs), what=f"gqa8 decode {kv} sharp={sharp}")
+    assert np.isfinite(got).all()
+
+
 def test_decode_8b_sharp_full():
     b = synth.make_decode_8b(seed=1, sharp=True)
     say("[decode-8b sharp] 256 decodes")
