@@ -14,7 +14,9 @@
 //    running (max, sum, output) state; the states are merged across lane
 //    groups with cross-lane shuffles and across waves through LDS. Each KV byte
 //    is read once for all G heads (grouped-query sharing). Arithmetic runs on
-//    the vector ALUs in fp32.
+//    the vector ALUs in fp32, except for groups of eight query heads (bf16 or
+//    fp8 KV, head_dim 128), whose products run on 16x16 bf16 MFMAs with the
+//    same item, split and merge structure (row_item_mfma).
 //  * Tile items (bf16 chunked prefill): 128 query rows (positions x group
 //    heads) of one chunk, causal against keys 0 .. last row's position. K and V
 //    are staged through LDS 64 keys at a time (V read back through transposing
