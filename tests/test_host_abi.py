@@ -12,6 +12,7 @@ import pytest
 import paper_2512_04013_amd as aug
 from paper_2512_04013_amd import AugError
 import synth
+from synth.attn_inputs import make_batch_from_lengths
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -192,6 +193,38 @@ def test_park_and_attention_reject_bad_arguments_without_touching_the_gpu():
     st = L.aug_attn_mixed(aug.C.byref(_shape(b)), aug.C.byref(info), None, 8, 8, 8, None, None, 8,
                           b.num_pool_blocks, 8, 8, 1 << 30, None)
     assert st == aug.AUG_ERR_INVALID
+
+
+def test_kv_append_rejects_bad_arguments_without_touching_the_gpu():
+    L = aug.lib()
+    b = synth.make_tiny_mixed(seed=0)
+    shape = _shape(b)
+    info, _ = aug.aug_attn_plan(shape, b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks)
+    assert info.num_append_items > 0
+    args = (8, 8, 8, 8, 8, None, None, 8, b.num_pool_blocks, None)
+    # NULL plan image / rows / cache
+    assert L.aug_kv_append(aug.C.byref(shape), aug.C.byref(info), None, *args[1:]) == aug.AUG_ERR_INVALID
+    assert L.aug_kv_append(aug.C.byref(shape), aug.C.byref(info), 8, None, *args[2:]) == aug.AUG_ERR_INVALID
+    # info that does not describe a plan image of this layout
+    bad = aug.aug_attn_plan_info.from_buffer_copy(info)
+    bad.plan_bytes += 16
+    assert L.aug_kv_append(aug.C.byref(shape), aug.C.byref(bad), *args) == aug.AUG_ERR_INVALID
+    bad = aug.aug_attn_plan_info.from_buffer_copy(info)
+    bad.num_append_items = -1
+    assert L.aug_kv_append(aug.C.byref(shape), aug.C.byref(bad), *args) == aug.AUG_ERR_INVALID
+    # fp8 cache without scales
+    s8 = aug.make_shape(64, 8, 128, "bf16", "fp8", "bf16", 0.088)
+    b8 = make_batch_from_lengths("a8", [3, 1], [40, 17], num_q_heads=64, num_kv_heads=8, head_dim=128,
+                                 q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16", n_pool_blocks=16, seed=1)
+    info8, _ = aug.aug_attn_plan(s8, b8.q_start, b8.ctx_len, b8.bt_start, b8.num_pool_blocks)
+    assert L.aug_kv_append(aug.C.byref(s8), aug.C.byref(info8), 8, 8, 8, 8, 8, None, None, 8, 16,
+                           None) == aug.AUG_ERR_INVALID
+    assert "scales" in aug.aug_last_error()
+    # an empty batch appends nothing and launches nothing
+    info0, _ = aug.aug_attn_plan(shape, [0], [], [0], b.num_pool_blocks)
+    assert info0.num_append_items == 0
+    assert L.aug_kv_append(aug.C.byref(shape), aug.C.byref(info0), None, None, None, None, None, None, None,
+                           None, b.num_pool_blocks, None) == aug.AUG_OK
 
 
 # ---- the former, bit-exact against the oracle --------------------------------------------
