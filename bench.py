@@ -200,6 +200,53 @@ def park_resume_rates(b, kv, log, reps: int = 3):
     return r
 
 
+def time_layers(n_layers, shape, info, plan_dev, k_new, v_new, q, pools, bids, num_pool_blocks, out, ws,
+                stream, log, reps: int = 20):
+    """One planned batch run as ``n_layers`` layers (per layer: the KV append
+    and the attention call, layer l on pool copy l mod copies), launched one
+    call at a time and as one captured HIP graph. Returns per-step and
+    per-layer times of both (medians over ``reps``)."""
+    import torch
+    import paper_2512_04013_amd as aug
+
+    def layers(st):
+        for l in range(n_layers):
+            kc, vc, ksc, vsc = pools[l % len(pools)]
+            aug.aug_kv_append(shape, info, plan_dev, k_new, v_new, kc, vc, ksc, vsc, bids, num_pool_blocks,
+                              stream=st)
+            aug.aug_attn_mixed(shape, info, plan_dev, q, kc, vc, ksc, vsc, bids, num_pool_blocks, out, ws,
+                               stream=st)
+
+    def timed(fn):
+        ts = []
+        for _ in range(reps + 3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts[3:]))
+
+    eager_ms = timed(lambda: layers(stream.cuda_stream))
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        layers(side.cuda_stream)
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        layers(torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    graph_ms = timed(g.replay)
+    log(f"{n_layers} layers: {eager_ms:.3f} ms launched one by one, {graph_ms:.3f} ms as one graph")
+    return {"n": n_layers, "what": "KV append + attention per layer, one plan, layer l on pool copy l mod copies",
+            "eager_ms_per_step": round(eager_ms, 4), "graph_ms_per_step": round(graph_ms, 4),
+            "eager_us_per_layer": round(1e3 * eager_ms / n_layers, 2),
+            "graph_us_per_layer": round(1e3 * graph_ms / n_layers, 2)}
+
+
 def make_workload(name: str, seed: int, log):
     """The workload's batch and the budget T_max it is formed under."""
     import synth
@@ -373,6 +420,10 @@ def main():
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--sweep-batches", type=int, default=200,
                     help="budget-sweep-fp8: formed batches replayed per budget")
+    ap.add_argument("--layers", type=int, default=8,
+                    help="after the steps, time this many layers of the planned batch (each an append and "
+                         "an attention call on its own pool copy) launched one by one and as one HIP graph "
+                         "(0: skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB a few times (a kernel of known "
                          "traffic for calibrating hardware byte counters)")
@@ -539,6 +590,9 @@ def main():
         "frac_hbm": round(app_bytes / (float(app_ms.mean()) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     if getattr(b, "park", None) is not None and len(b.park.resume_blocks) and not args.no_park_resume:
         result["park_resume"] = park_resume_rates(b, kv, log)
+    if args.layers > 0:
+        result["layers"] = time_layers(args.layers, shape, info, plan_dev, k_new, v_new, q, pools, bids,
+                                       kv.num_pool_blocks, out, ws_dev, stream, log)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(b, args.cpu_budget_s)

@@ -203,8 +203,12 @@ aug_status aug_attn_mixed(const aug_attn_shape* shape, const aug_attn_plan_info*
  * re-encoded as enc(dec(code) * old / new); new tokens are enc(x / scale)
  * (0 if the scale is 0). enc rounds to nearest even and saturates at +-448;
  * products and quotients are single float32 operations in that order.
- * A block id outside the pool is skipped. Enqueued on `stream` as one kernel
- * launch (none for an empty batch).
+ * A block id outside the pool is skipped. The blocks that receive tokens
+ * must be distinct across the batch (aug_attn_plan checks this when it is
+ * given the host block table); two requests appending into one block would
+ * race on its contents and scale. Enqueued on `stream` as one kernel launch
+ * (none for an empty batch); no allocation, no memset, so the call can be
+ * captured in a HIP graph and replayed.
  * Errors: AUG_ERR_INVALID (NULL pointers, info/shape mismatch,
  * missing scales for fp8), AUG_ERR_HIP (launch). */
 aug_status aug_kv_append(const aug_attn_shape* shape, const aug_attn_plan_info* info,

@@ -76,23 +76,32 @@ class MixedAttention:
         out_dtype = torch.float32 if shape.out_dtype == 0 else torch.bfloat16
         self.out = torch.empty((rows, shape.num_q_heads, shape.head_dim), dtype=out_dtype, device=device)
 
-    def run(self, q: torch.Tensor, stream=None):
-        aug_attn_mixed(self.shape, self.info, self.plan_dev, q, self.kv.k_cache, self.kv.v_cache,
-                       self.kv.k_scale, self.kv.v_scale, self.block_ids, self.kv.num_pool_blocks,
-                       self.out, self.workspace, stream=stream)
-        return self.out
+    def run(self, q: torch.Tensor, stream=None, kv: "PagedKV" = None, block_ids: torch.Tensor = None,
+            out: torch.Tensor = None):
+        """Enqueue the batch's attention. ``kv``, ``block_ids`` and ``out``
+        default to the planned ones; another layer of the same batch passes its
+        own pool, block ids (same table shape) and output, and reuses the plan."""
+        kv = self.kv if kv is None else kv
+        out = self.out if out is None else out
+        aug_attn_mixed(self.shape, self.info, self.plan_dev, q, kv.k_cache, kv.v_cache,
+                       kv.k_scale, kv.v_scale, self.block_ids if block_ids is None else block_ids,
+                       kv.num_pool_blocks, out, self.workspace, stream=stream)
+        return out
 
-    def append(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None):
-        """Write the batch's new K/V rows ([rows][H_kv][D]) into the pool."""
+    def append(self, k_new: torch.Tensor, v_new: torch.Tensor, stream=None, kv: "PagedKV" = None,
+               block_ids: torch.Tensor = None):
+        """Write the batch's new K/V rows ([rows][H_kv][D]) into the pool
+        (``kv`` and ``block_ids`` as for ``run``)."""
+        kv = self.kv if kv is None else kv
         want = (int(self.info.total_rows), self.shape.num_kv_heads, self.shape.head_dim)
         dtype = torch.float32 if self.shape.kv_dtype == 0 else torch.bfloat16
         for t in (k_new, v_new):
             if tuple(t.shape) != want or t.dtype != dtype or not t.is_contiguous():
                 raise ValueError(f"new K/V rows must be contiguous {dtype} of shape {want}, got "
                                  f"{t.dtype} {tuple(t.shape)}")
-        aug_kv_append(self.shape, self.info, self.plan_dev, k_new, v_new, self.kv.k_cache,
-                      self.kv.v_cache, self.kv.k_scale, self.kv.v_scale, self.block_ids,
-                      self.kv.num_pool_blocks, stream=stream)
+        aug_kv_append(self.shape, self.info, self.plan_dev, k_new, v_new, kv.k_cache,
+                      kv.v_cache, kv.k_scale, kv.v_scale, self.block_ids if block_ids is None else block_ids,
+                      kv.num_pool_blocks, stream=stream)
 
 
 def shape_of(batch) -> object:
