@@ -562,6 +562,12 @@ def main():
                 "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(b.name)}
         if flops > 0:
             roof["prefill_mfma_tflops"] = round(achieved_tfs, 2)
+    # decode rows' flops (4 D H_q per key): on the vector ALUs for up to four
+    # heads per KV head, on MFMA for eight; reported beside the HBM figure
+    dec_flops = 4.0 * b.head_dim * b.num_q_heads * float(b.ctx_len[b.q_len == 1].sum())
+    if dec_flops > 0:
+        roof["decode_tflops"] = round(dec_flops / (attn_ms * 1e-3) / 1e12, 2)
+        roof["decode_tflops_frac_of_fp32_valu"] = round(dec_flops / (attn_ms * 1e-3) / 157.3e12, 4)
     roof.update({"kernel": "aug_attn_mixed launches (attention + split-K merge)",
                  "algorithmic_bytes_per_launch": int(nbytes), "prefill_flops_per_launch": int(flops),
                  "launch_ms": round(attn_ms, 4), "launch_ms_median": round(float(np.median(launch_ms)), 4),
