@@ -372,7 +372,10 @@ def budget_sweep(args, log):
                            "attn_query_tokens_per_s": round(qsum / t, 1), "step_query_tokens_per_s": round(qsum / wall, 1),
                            "hbm_frac": round(nbytes / t / (HBM_PEAK_GBS * 1e9), 4),
                            "mfma_frac": round(nflops / t / (MFMA_BF16_PEAK_TFS * 1e12), 4),
-                           "attn_ms_per_batch": round(1e3 * t / len(pick), 4)}
+                           "attn_ms_per_batch": round(1e3 * t / len(pick), 4),
+                           # the library former's own time per iteration over the whole trace
+                           # (the paper's per-iteration scheduling overhead, Table 3)
+                           "former_per_iteration": run.former_stats}
         log(f"budget {budget}: {results[budget]}")
         t_all += t
         wall_all += wall

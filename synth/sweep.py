@@ -51,6 +51,7 @@ class SweepRun:
     finished: int                    # requests that finished
     sim_seconds: float
     metrics: dict                    # request-level results (ServingLoop.metrics)
+    former_stats: Optional[dict] = None   # per-iteration former time, when the former records it
 
 
 def run_budget(budget: int, former: Callable, lifecycle, seed: int = 0, dynamic: bool = True,
@@ -69,7 +70,32 @@ def run_budget(budget: int, former: Callable, lifecycle, seed: int = 0, dynamic:
     steps = [s for s in loop.steps if s.ids]
     return SweepRun(budget=budget, dynamic=dynamic, steps=steps,
                     complete=len(loop.done) == n_requests, finished=len(loop.done),
-                    sim_seconds=loop.now, metrics=dict(loop.metrics(), preemptions=loop.preemptions))
+                    sim_seconds=loop.now, metrics=dict(loop.metrics(), preemptions=loop.preemptions),
+                    former_stats=former_overhead(getattr(former, "timings", None)))
+
+
+# bins of paused requests for the per-iteration former time (the paper's
+# scheduling-overhead table groups iterations the same way)
+PAUSED_BINS = ((0, 50), (50, 100), (100, 150), (150, 200), (200, 10 ** 9))
+
+
+def former_overhead(timings) -> Optional[dict]:
+    """Per-iteration time of the former call (mean, p50, p99, in us), overall
+    and by number of paused requests, from (seconds, records, paused) tuples."""
+    if not timings:
+        return None
+    t = np.array([x[0] for x in timings]) * 1e6
+    n = np.array([x[1] for x in timings])
+    pz = np.array([x[2] for x in timings])
+    out = {"iterations": int(t.size), "us_mean": round(float(t.mean()), 1),
+           "us_p50": round(float(np.median(t)), 1), "us_p99": round(float(np.percentile(t, 99)), 1),
+           "records_mean": round(float(n.mean()), 1), "records_max": int(n.max()), "by_paused": {}}
+    for lo, hi in PAUSED_BINS:
+        sel = (pz >= lo) & (pz < hi)
+        if sel.any():
+            key = f"{lo}-{hi}" if hi < 10 ** 9 else f">={lo}"
+            out["by_paused"][key] = {"iterations": int(sel.sum()), "us_mean": round(float(t[sel].mean()), 1)}
+    return out
 
 
 def prefill_pairs(step: StepRecord) -> int:
