@@ -122,12 +122,16 @@ def test_gqa8_decode_batch_full_size(kv, sharp):
     contexts lognormal (median 2500, sigma 0.8, cap 16384): the 8-way grouped
     decode rows run on the MFMA row path. Every row of a sample of 64
     requests (and the shortest and longest) against the oracle."""
-    rng = np.random.default_rng(21)
-    ctx = np.clip(np.rint(rng.lognormal(np.log(2500), 0.8, 512)), 1, 16384).astype(int)
-    b = make_batch_from_lengths("gqa8-decode", [1] * 512, ctx.tolist(), num_q_heads=64, num_kv_heads=8,
-                                head_dim=128, q_dtype="bf16", kv_dtype=kv, out_dtype="bf16",
-                                n_pool_blocks=int(sum(-(-c // 16) for c in ctx)) + 64, seed=22,
-                                kv_std=1.0 if sharp else 1.0 / np.sqrt(128.0))
+    if kv == "fp8":
+        b = synth.make_decode_gqa8_fp8(seed=0, sharp=sharp)      # the decode-fp8-64x8 bench workload
+        ctx = b.ctx_len.astype(int)
+    else:
+        rng = np.random.default_rng(21)
+        ctx = np.clip(np.rint(rng.lognormal(np.log(2500), 0.8, 512)), 1, 16384).astype(int)
+        b = make_batch_from_lengths("gqa8-decode", [1] * 512, ctx.tolist(), num_q_heads=64, num_kv_heads=8,
+                                    head_dim=128, q_dtype="bf16", kv_dtype=kv, out_dtype="bf16",
+                                    n_pool_blocks=int(sum(-(-c // 16) for c in ctx)) + 64, seed=22,
+                                    kv_std=1.0 if sharp else 1.0 / np.sqrt(128.0))
     say(f"[gqa8 decode] kv={kv} sharp={sharp} keys={int(ctx.sum())}")
     got, att = _run(b)
     reqs = sorted(set([int(np.argmin(ctx)), int(np.argmax(ctx))] +
