@@ -171,6 +171,24 @@ def test_ssjf_ranks_by_predicted_output_then_arrival():
     assert plan.ids == [4, 5, 2, 1, 0, 3]
 
 
+def test_prefill_takes_one_chunk_capped_by_chunk_cap_and_budget():
+    # a 1500-token prompt runs 512 tokens per iteration; with a 300-token
+    # budget the chunk is cut to the budget, so it can still run alone
+    r = Request(id=0, arrival=0.0, state=WAITING, seg_prefill=1500, pending=1500, pred_out=10)
+    plan = of.form_batch([r], free_blocks=10**6, block_size=16, now=1.0,
+                         p=Params(t_max=2048, beta_low=1, beta_high=1, chunk_cap=512))
+    assert plan.q_len == [512]
+    plan = of.form_batch([r], free_blocks=10**6, block_size=16, now=1.0,
+                         p=Params(t_max=300, beta_low=1, beta_high=1, chunk_cap=512))
+    assert plan.budget == 300 and plan.q_len == [300]
+    # the last chunk takes what is left
+    r2 = Request(id=1, arrival=0.0, state=RUNNING, seg_prefill=1500, ctx_len=1024, pending=476,
+                 blocks_on_gpu=64, pred_out=10)
+    plan = of.form_batch([r2], free_blocks=10**6, block_size=16, now=1.0,
+                         p=Params(t_max=2048, beta_low=1, beta_high=1, chunk_cap=512))
+    assert plan.q_len == [476]
+
+
 # ---- packing ---------------------------------------------------------------------------
 
 def _mixed_2048_requests(extra_decode=False):
