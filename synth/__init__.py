@@ -17,6 +17,8 @@ from .attn_inputs import (  # noqa: F401
     make_mixed_8b,
     make_long_context,
     make_decode_gqa8_fp8,
+    make_prefill_8b,
+    make_prefill_gqa8_fp8,
     make_batch_from_lengths,
     make_new_kv,
     poison_new_slots,

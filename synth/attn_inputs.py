@@ -452,6 +452,36 @@ def make_decode_gqa8_fp8(seed: int = 0, sharp: bool = False, n_req: int = 512) -
         kv_std=1.0 if sharp else 1.0 / np.sqrt(128.0))
 
 
+def make_prefill_8b(seed: int = 0, sharp: bool = False, n_chunks: int = 8, chunk: int = 512) -> AttnBatch:
+    """A prefill-only batch on the 8B layer (32/8 heads, head_dim 128, bf16):
+    ``n_chunks`` chunks of ``chunk`` rows, each behind a prior context drawn
+    U{0..4096}, the prefill part of the mixed batch at a 4096-token budget."""
+    rng = np.random.default_rng(seed)
+    ctx = chunk + rng.integers(0, 4097, size=n_chunks)
+    # room beside the batch for the memory-derived budget to reach 4096 tokens
+    pool = int(((ctx + BLOCK - 1) // BLOCK).sum()) * 5 // 4 + 1024
+    return make_batch_from_lengths(
+        "prefill-8b-bf16", [chunk] * n_chunks, ctx.tolist(), num_q_heads=32, num_kv_heads=8, head_dim=128,
+        q_dtype="bf16", kv_dtype="bf16", out_dtype="bf16", n_pool_blocks=pool, seed=seed + 3000,
+        kv_std=1.0 if sharp else 1.0 / np.sqrt(128.0))
+
+
+def make_prefill_gqa8_fp8(seed: int = 0, sharp: bool = False, n_chunks: int = 16, chunk: int = 512) -> AttnBatch:
+    """The prefill-dominated end of the batches an 8192-token budget forms on
+    the budget sweep's layer (64/8 heads, head_dim 128, bf16 Q, fp8 E4M3FN KV
+    with per-block scales): ``n_chunks`` chunks of ``chunk`` rows, each behind
+    a prior context drawn U{0..2048} (prompts of the trace have a median of
+    800 tokens, so most chunks sit one to four chunks into their prompt)."""
+    rng = np.random.default_rng(seed)
+    ctx = chunk + rng.integers(0, 2049, size=n_chunks)
+    # room beside the batch for the memory-derived budget to reach 8192 tokens
+    pool = int(((ctx + BLOCK - 1) // BLOCK).sum()) * 5 // 4 + 1024
+    return make_batch_from_lengths(
+        "prefill-fp8-64x8", [chunk] * n_chunks, ctx.tolist(), num_q_heads=64, num_kv_heads=8, head_dim=128,
+        q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16", n_pool_blocks=pool, seed=seed + 4000,
+        kv_std=1.0 if sharp else 1.0 / np.sqrt(128.0))
+
+
 def make_config(cfg: int, seed: int = 0, sharp: bool = False, **kw) -> AttnBatch:
     if cfg == 1:
         return make_tiny_mixed(seed, **kw)

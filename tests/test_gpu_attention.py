@@ -246,3 +246,23 @@ def test_long_context_sampled():
     want = oa.attention_for(b, requests=reqs, k_cache=k_res, v_cache=v_res)
     compare(got, want, "bf16", rows=rows_of(b, reqs), what=f"long-context reqs={reqs}")
     assert np.isfinite(got).all()
+
+
+@pytest.mark.parametrize("workload,sharp", [("prefill-fp8-64x8", False), ("prefill-fp8-64x8", True),
+                                             ("prefill-8b", False)])
+def test_prefill_workloads_full_size_sampled(workload, sharp):
+    """The prefill-dominated benchmark batches at full size, in the launch
+    configuration the benchmark times (automatic split): 16 x 512-row chunks
+    on the 64/8-head fp8 layer, 8 x 512-row chunks on the 8B bf16 layer.
+    Every row of the chunks with the shortest and the longest prior context,
+    and of one more, against the oracle."""
+    b = (synth.make_prefill_gqa8_fp8 if workload == "prefill-fp8-64x8" else synth.make_prefill_8b)(
+        seed=0, sharp=sharp)
+    ctx = b.ctx_len.astype(int)
+    say(f"[{workload}] sharp={sharp} {b.num_reqs} chunks, {b.total_q} rows, keys={int(ctx.sum())}")
+    got, att = _run(b)
+    assert att.info.num_prefill_items > 0
+    reqs = sorted({int(np.argmin(ctx)), int(np.argmax(ctx)), b.num_reqs // 2})
+    want = oa.attention_for(b, requests=reqs)
+    compare(got, want, "bf16", rows=rows_of(b, reqs), what=f"{workload} sharp={sharp} reqs={reqs}")
+    assert np.isfinite(got).all()
