@@ -18,6 +18,7 @@
  *                     (Eqs. cost, c_fb, c_ik_new, value, theta), Waste policy
  *                     choice (Appendix B) and greedy packing (Algorithm 1 (4))
  *   aug_attn_plan     host: validates a formed batch and writes the work list
+ *   aug_plan_upload   pinned host -> device: the work list, on the launch stream
  *   aug_kv_append     device: the step's new K/V rows into their paged slots
  *   aug_attn_mixed    device: one launch of paged, causal, grouped-query
  *                     attention over every chunked-prefill row and decode row
@@ -153,6 +154,20 @@ typedef struct {
 aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batch,
                          int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
                          aug_attn_plan_info* info);
+
+/* Copy `bytes` bytes of a plan image (or any other bytes) from pinned host
+ * memory host_src to device memory dev_dst with one small copy kernel
+ * enqueued on `stream`, so that the copy starts as soon as the stream's
+ * previous kernel has finished instead of waiting for a DMA engine; the step's
+ * launches queued after it on the same stream see the bytes. host_src must be
+ * page-locked memory registered with HIP (hipHostMalloc, torch's pinned
+ * tensors) and must stay unchanged until the copy has run; both ranges must
+ * lie inside their allocations (the caller's duty: they are not checked); both
+ * pointers 16-byte aligned. bytes == 0 enqueues nothing. No allocation, no
+ * memset.
+ * Errors: AUG_ERR_INVALID (NULL or misaligned pointer, host_src not pinned
+ * host memory, dev_dst not device memory), AUG_ERR_HIP (launch). */
+aug_status aug_plan_upload(const void* host_src, void* dev_dst, size_t bytes, void* stream);
 
 /* Mixed-batch paged attention: for every row of every request of the planned
  * batch, O = softmax(softmax_scale * q K^T, causal) V over the request's

@@ -30,9 +30,9 @@ AUG_POL_NONE, AUG_PRESERVE, AUG_DISCARD, AUG_SWAP = 0, 1, 2, 3
 
 DTYPE_CODES = {"f32": AUG_F32, "bf16": AUG_BF16, "fp8": AUG_FP8_E4M3FN}
 
-EXPORTED = ["aug_request_arrive", "aug_request_return", "aug_attn_plan", "aug_attn_mixed", "aug_kv_append", "aug_kv_record_bytes", "aug_kv_park",
-            "aug_kv_resume", "aug_form_batch", "aug_status_string", "aug_last_error",
-            "aug_abi_version"]
+EXPORTED = ["aug_request_arrive", "aug_request_return", "aug_attn_plan", "aug_plan_upload", "aug_attn_mixed",
+            "aug_kv_append", "aug_kv_record_bytes", "aug_kv_park", "aug_kv_resume", "aug_form_batch",
+            "aug_status_string", "aug_last_error", "aug_abi_version"]
 
 
 class AugError(RuntimeError):
@@ -119,6 +119,7 @@ def lib():
                                  P, P, P, C.c_int32, P, P, C.c_size_t, P]
     L.aug_kv_append.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P, P,
                                 P, P, P, C.c_int32, P]
+    L.aug_plan_upload.argtypes = [P, P, C.c_size_t, P]
     L.aug_kv_record_bytes.argtypes = [C.POINTER(aug_attn_shape)]
     L.aug_kv_record_bytes.restype = C.c_size_t
     L.aug_kv_park.argtypes = [C.POINTER(aug_attn_shape), P, P, P, P, P, P, C.c_int32, C.c_int32, P,
@@ -129,7 +130,7 @@ def lib():
                                  C.POINTER(aug_batch_plan)]
     L.aug_request_arrive.argtypes = [P, C.c_int64, C.c_double, C.c_int32, C.c_int32, C.c_double, C.c_int32]
     L.aug_request_return.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_double, C.c_int32]
-    for f in ("aug_attn_plan", "aug_attn_mixed", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
+    for f in ("aug_attn_plan", "aug_plan_upload", "aug_attn_mixed", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
               "aug_form_batch", "aug_request_arrive", "aug_request_return"):
         getattr(L, f).restype = C.c_int
     L.aug_status_string.argtypes = [C.c_int]
@@ -221,6 +222,16 @@ def aug_attn_plan(shape: aug_attn_shape, q_start, ctx_len, bt_start, num_pool_bl
 
 
 _plan_buf = np.zeros(1 << 20, dtype=np.uint8)
+
+
+def aug_plan_upload(host_src, dev_dst, nbytes: Optional[int] = None, stream=None):
+    """Enqueue the copy of ``nbytes`` bytes (default: all of ``host_src``)
+    from a pinned host tensor to a device tensor by the library's copy kernel
+    on ``stream`` (default: the current stream of ``dev_dst``)."""
+    if nbytes is None:
+        nbytes = host_src.numel() * host_src.element_size()
+    st = _stream(stream, dev_dst, dev_dst)
+    _check(lib().aug_plan_upload(_ptr(host_src), _ptr(dev_dst), int(nbytes), st), "aug_plan_upload")
 
 
 def aug_attn_mixed(shape: aug_attn_shape, info: aug_attn_plan_info, plan_dev, q, k_cache, v_cache,

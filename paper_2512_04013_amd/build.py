@@ -24,7 +24,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libaug.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-HIP_SOURCES = ["attn.hip", "kvappend.hip", "kvpark.hip"]
+HIP_SOURCES = ["attn.hip", "kvappend.hip", "kvpark.hip", "upload.hip"]
 CPP_SOURCES = ["plan.cpp", "former.cpp", "status.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall", "-Wno-unused-function"]

@@ -13,7 +13,7 @@ import numpy as np
 import torch
 
 from . import (aug_attn_mixed, aug_attn_plan, aug_kv_append, aug_kv_park, aug_kv_record_bytes, aug_kv_resume,
-               make_shape)
+               aug_plan_upload, make_shape)
 
 _TORCH_STORAGE = {"f32": torch.float32, "bf16": torch.bfloat16, "fp8": torch.uint8}
 
@@ -68,9 +68,11 @@ class MixedAttention:
         self.info, plan = aug_attn_plan(shape, q_start, ctx_len, bt_start, kv.num_pool_blocks,
                                         block_ids_host if check_blocks else None,
                                         kv_split_tokens=kv_split_tokens)
+        # pinned staging kept alive with the batch; the library's copy kernel
+        # moves it on the current stream of the cache's device
         self.plan_host = torch.from_numpy(plan.copy()).pin_memory()
         self.plan_dev = torch.empty(max(1, plan.size), dtype=torch.uint8, device=device)
-        self.plan_dev[:plan.size].copy_(self.plan_host, non_blocking=True)
+        aug_plan_upload(self.plan_host, self.plan_dev, plan.size)
         self.workspace = torch.empty(max(256, int(self.info.workspace_bytes)), dtype=torch.uint8,
                                      device=device)
         self.block_ids = block_ids_dev

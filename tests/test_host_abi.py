@@ -227,6 +227,19 @@ def test_kv_append_rejects_bad_arguments_without_touching_the_gpu():
                            None, b.num_pool_blocks, None) == aug.AUG_OK
 
 
+def test_plan_upload_rejects_bad_arguments_without_touching_the_gpu():
+    L = aug.lib()
+    # nothing to copy: nothing enqueued, whatever the pointers
+    assert L.aug_plan_upload(None, None, 0, None) == aug.AUG_OK
+    assert L.aug_plan_upload(None, 4096, 16, None) == aug.AUG_ERR_INVALID
+    assert L.aug_plan_upload(4096, None, 16, None) == aug.AUG_ERR_INVALID
+    assert "NULL" in aug.aug_last_error()
+    # both pointers must be 16-byte aligned
+    assert L.aug_plan_upload(4096 + 8, 8192, 64, None) == aug.AUG_ERR_INVALID
+    assert L.aug_plan_upload(4096, 8192 + 4, 64, None) == aug.AUG_ERR_INVALID
+    assert "aligned" in aug.aug_last_error()
+
+
 # ---- the former, bit-exact against the oracle --------------------------------------------
 
 from oracle import former as of  # noqa: E402
