@@ -139,17 +139,21 @@ def cpu_baseline(b, budget_s: float = 15.0):
     except Exception:  # noqa: BLE001
         threads = len(os.sched_getaffinity(0))
     order = list(range(b.num_reqs))
-    done_rows, t_used, n_done = 0, 0.0, 0
+    elem = {"f32": 4, "bf16": 2, "fp8": 1}[b.kv_dtype]
+    kv_per_token = 2 * b.num_kv_heads * b.head_dim * elem     # K and V bytes of one context token
+    done_rows, t_used, n_done, kv_bytes = 0, 0.0, 0, 0
     for r in order:
         t0 = time.perf_counter()
         oa.attention_for(b, requests=[r])
         t_used += time.perf_counter() - t0
         done_rows += int(b.q_len[r])
+        kv_bytes += int(b.ctx_len[r]) * kv_per_token
         n_done += 1
         if t_used >= budget_s:
             break
     res = {"value": done_rows / t_used, "unit": "query-tokens/s", "cores": int(threads),
-           "kind": "oracle",
+           "affinity_cores": len(os.sched_getaffinity(0)),
+           "kv_gbs": round(kv_bytes / t_used / 1e9, 4), "kind": "oracle",
            "sample": f"first {n_done} of {b.num_reqs} requests ({done_rows} query rows), float64 numpy, "
                      f"{t_used:.1f} s"}
     # the same sample again with numpy's BLAS held to one thread
