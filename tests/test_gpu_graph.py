@@ -1,6 +1,6 @@
-"""Several layers of one planned batch (KV append, then attention, per layer,
-each layer with its own pool, block table, queries and new rows) captured in
-a HIP graph: every replay reproduces the eager launches bit for bit, with the
+"""The plan upload and several layers of one planned batch (KV append, then
+attention, per layer, each layer with its own pool, block table, queries and
+new rows) captured in a HIP graph: every replay reproduces the eager launches bit for bit, with the
 program's own eager work and synchronisations between replays."""
 
 import numpy as np
@@ -8,6 +8,7 @@ import pytest
 
 torch = pytest.importorskip("torch")
 
+import paper_2512_04013_amd as aug  # noqa: E402
 import synth  # noqa: E402
 from oracle import attention as oa  # noqa: E402
 from oracle import kvappend  # noqa: E402
@@ -48,7 +49,11 @@ def test_layers_in_a_graph_replay_the_eager_bits(kv):
         f"groups={att.info.num_merge_groups} tile merges={att.info.num_tile_merge_groups}")
     assert att.info.num_merge_groups > att.info.num_tile_merge_groups > 0
 
+    plan_bytes = int(att.info.plan_bytes)
+
     def one_step(stream=None):
+        # the step's plan image from its pinned host copy, then every layer
+        aug.aug_plan_upload(att.plan_host, att.plan_dev, plan_bytes, stream=stream)
         for L in layers:
             att.append(L["k_new"], L["v_new"], stream=stream, kv=L["pool"], block_ids=L["bids"])
             att.run(L["q"], stream=stream, kv=L["pool"], block_ids=L["bids"], out=L["out"])
