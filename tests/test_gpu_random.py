@@ -39,16 +39,44 @@ def _random_lengths(rng, n_req):
     return q, c
 
 
+def _wide_lengths(rng, n_req):
+    """Longer chunks (up to 512 rows, at and around the planner's tile and
+    chunk sizes) and long decodes (up to 12k keys, several split spans)."""
+    q, c = [], []
+    for _ in range(n_req):
+        kind = rng.integers(0, 3)
+        if kind == 0:
+            qq, prior = 1, int(rng.choice([int(rng.integers(0, 12000)), 4095, 4096, 8191]))
+        elif kind == 1:
+            qq = int(rng.choice([255, 256, 257, 383, 511, 512]))
+            prior = int(rng.choice([0, 16, 1023, int(rng.integers(0, 2500))]))
+        else:
+            qq = int(rng.integers(2, 130))
+            prior = int(rng.integers(0, 6000))
+        q.append(qq)
+        c.append(qq + prior)
+    return q, c
+
+
 @pytest.mark.parametrize("case", range(24))
 def test_random_batch_after_append(case):
+    _check_random_case(case, 1000 + case, _random_lengths, [0, 16, 64, 512])
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_wide_random_batch_after_append(case):
+    _check_random_case(case, 5000 + case, _wide_lengths, [0, 0, 256, 1024, 3000])
+
+
+def _check_random_case(case, seed, lengths, splits):
     from paper_2512_04013_amd import runtime as rt
-    rng = np.random.default_rng(1000 + case)
+    rng = np.random.default_rng(seed)
     hq, hkv, d, kv = SHAPES[case % len(SHAPES)]
     qd = "f32" if kv == "f32" else "bf16"
-    q_lens, ctx_lens = _random_lengths(rng, int(rng.integers(1, 9)))
-    split = int(rng.choice([0, 16, 64, 512]))
+    q_lens, ctx_lens = lengths(rng, int(rng.integers(1, 9)))
+    split = int(rng.choice(splits))
     sharp = bool(rng.integers(0, 2))
-    say(f"[random] case={case} heads={hq}/{hkv} d={d} kv={kv} q={q_lens} ctx={ctx_lens} split={split} sharp={sharp}")
+    say(f"[random] seed={seed} case={case} heads={hq}/{hkv} d={d} kv={kv} q={q_lens} ctx={ctx_lens} split={split} sharp={sharp}")
     pool = int(sum(-(-c // 16) for c in ctx_lens)) + 32
     b = make_batch_from_lengths("random", q_lens, ctx_lens, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
                                 q_dtype=qd, kv_dtype=kv, out_dtype=qd, n_pool_blocks=pool, seed=case,
@@ -66,5 +94,5 @@ def test_random_batch_after_append(case):
     assert np.array_equal(kvp.k_cache.contiguous().view(torch.uint8).cpu().numpy().reshape(-1),
                           np.ascontiguousarray(k).view(np.uint8).reshape(-1))
     want = oa.attention_for(b, k_cache=k, v_cache=v, k_scale=ks, v_scale=vs)
-    compare(got, want, qd, what=f"random case {case} items={att.info.num_items} tiles={att.info.num_prefill_items} "
+    compare(got, want, qd, what=f"random seed {seed} items={att.info.num_items} tiles={att.info.num_prefill_items} "
                                 f"groups={att.info.num_merge_groups}")
