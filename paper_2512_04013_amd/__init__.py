@@ -16,6 +16,7 @@ from __future__ import annotations
 
 import ctypes as C
 import os
+import threading
 from typing import Optional
 
 import numpy as np
@@ -210,18 +211,21 @@ def aug_attn_plan(shape: aug_attn_shape, q_start, ctx_len, bt_start, num_pool_bl
                           bs.ctypes.data_as(p32), None if bi is None else bi.ctypes.data_as(p32),
                           int(num_pool_blocks))
     info = aug_attn_plan_info()
-    global _plan_buf
+    # one scratch image per thread: ctypes releases the GIL during the call
+    buf = getattr(_plan_scratch, "buf", None)
+    if buf is None:
+        buf = _plan_scratch.buf = np.zeros(1 << 20, dtype=np.uint8)
     while True:
-        st = L.aug_attn_plan(C.byref(shape), C.byref(desc), int(kv_split_tokens), _plan_buf.ctypes.data,
-                             _plan_buf.nbytes, C.byref(info))
-        if st == AUG_ERR_NO_SPACE and info.plan_bytes > _plan_buf.nbytes:
-            _plan_buf = np.zeros(int(info.plan_bytes) * 2, dtype=np.uint8)
+        st = L.aug_attn_plan(C.byref(shape), C.byref(desc), int(kv_split_tokens), buf.ctypes.data,
+                             buf.nbytes, C.byref(info))
+        if st == AUG_ERR_NO_SPACE and info.plan_bytes > buf.nbytes:
+            buf = _plan_scratch.buf = np.zeros(int(info.plan_bytes) * 2, dtype=np.uint8)
             continue
         _check(st, "aug_attn_plan")
-        return info, _plan_buf[:int(info.plan_bytes)].copy()
+        return info, buf[:int(info.plan_bytes)].copy()
 
 
-_plan_buf = np.zeros(1 << 20, dtype=np.uint8)
+_plan_scratch = threading.local()
 
 
 def aug_plan_upload(host_src, dev_dst, nbytes: Optional[int] = None, stream=None):

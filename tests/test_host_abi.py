@@ -227,6 +227,32 @@ def test_kv_append_rejects_bad_arguments_without_touching_the_gpu():
                            None, b.num_pool_blocks, None) == aug.AUG_OK
 
 
+def test_planning_from_several_threads_gives_the_serial_plans():
+    """The binding releases the GIL inside the planner; plans made on eight
+    threads at once must equal the plans made one after another."""
+    import threading
+    batches = [synth.make_tiny_mixed(seed=s) for s in range(4)] + \
+              [synth.make_mixed_8b(seed=s, n_dec=48, n_pre=2, n_pool_blocks=16384) for s in range(4)]
+    want = [aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks, b.block_ids)[1]
+            for b in batches]
+    bad = []
+
+    def worker(k):
+        b = batches[k]
+        for _ in range(30):
+            _, plan = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
+                                        b.block_ids)
+            if not np.array_equal(plan, want[k]):
+                bad.append(k)
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(len(batches))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not bad
+
+
 def test_plan_upload_rejects_bad_arguments_without_touching_the_gpu():
     L = aug.lib()
     # nothing to copy: nothing enqueued, whatever the pointers
