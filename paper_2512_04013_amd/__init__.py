@@ -303,24 +303,31 @@ def former_params(beta=5e-5, t_max=2048, beta_low=0.5, beta_high=2.0, chunk_cap=
                              int(skip_instead_of_break), int(order), 0)
 
 
+_former_scratch = threading.local()
+
+
+def _former_outputs(cap: int):
+    """The calling thread's output arrays of aug_form_batch (at least ``cap``
+    entries each) and the aug_batch_plan pointing at them, reused across
+    calls; callers copy what they return."""
+    sc = getattr(_former_scratch, "v", None)
+    if sc is None or sc[-1].cap < cap:
+        cap = max(cap, 64 if sc is None else 2 * sc[-1].cap)
+        arrs = [np.zeros(cap, t) for t in (np.int64, np.int32, np.float64, np.int64, np.int64, np.int64,
+                                            np.int32, np.float64)]
+        P64, P32, PD = C.POINTER(C.c_int64), C.POINTER(C.c_int32), C.POINTER(C.c_double)
+        ptrs = [a.ctypes.data_as(pt) for a, pt in zip(arrs, (P64, P32, PD, P64, P64, P64, P32, PD))]
+        sc = _former_scratch.v = (*arrs, aug_batch_plan(cap, 0, 0, 0, 0, 0, *ptrs))
+    return sc
+
+
 def aug_form_batch(reqs: np.ndarray, free_blocks: int, now: float, params: aug_former_params):
     """Form one batch from a structured array of REQUEST_DTYPE. Returns a dict
     with budget, ids, q_len, theta, resume_ids, park_ids, free_ids, policy, cost."""
     reqs = np.ascontiguousarray(reqs, dtype=REQUEST_DTYPE)
     n = len(reqs)
-    cap = max(n, 1)
-    ids = np.zeros(cap, np.int64)
-    q_len = np.zeros(cap, np.int32)
-    theta = np.zeros(cap, np.float64)
-    res = np.zeros(cap, np.int64)
-    park = np.zeros(cap, np.int64)
-    free = np.zeros(cap, np.int64)
-    pol = np.zeros(cap, np.int32)
-    cost = np.zeros(cap, np.float64)
-    P64, P32, PD = C.POINTER(C.c_int64), C.POINTER(C.c_int32), C.POINTER(C.c_double)
-    out = aug_batch_plan(cap, 0, 0, 0, 0, 0, ids.ctypes.data_as(P64), q_len.ctypes.data_as(P32),
-                         theta.ctypes.data_as(PD), res.ctypes.data_as(P64), park.ctypes.data_as(P64),
-                         free.ctypes.data_as(P64), pol.ctypes.data_as(P32), cost.ctypes.data_as(PD))
+    ids, q_len, theta, res, park, free, pol, cost, out = _former_outputs(max(n, 1))
+    out.budget = out.n_sched = out.n_resume = out.n_park = out.n_free = 0
     _check(lib().aug_form_batch(reqs.ctypes.data if n else None, n, int(free_blocks), float(now),
                                 C.byref(params), C.byref(out)), "aug_form_batch")
     k = out.n_sched
