@@ -266,3 +266,33 @@ def test_prefill_workloads_full_size_sampled(workload, sharp):
     want = oa.attention_for(b, requests=reqs)
     compare(got, want, "bf16", rows=rows_of(b, reqs), what=f"{workload} sharp={sharp} reqs={reqs}")
     assert np.isfinite(got).all()
+
+
+def test_long_chunk_over_long_prior_context():
+    """One 1024-row chunk behind 16,000 cached tokens (tiles split along
+    keys, merged by the tile merge launch) next to two decodes, every row
+    against the oracle."""
+    q_lens, ctx_lens = [1024, 1, 1], [17024, 9000, 3]
+    b = make_batch_from_lengths("long-chunk", q_lens, ctx_lens, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                                q_dtype="bf16", kv_dtype="bf16", out_dtype="bf16",
+                                n_pool_blocks=int(sum(-(-c // 16) for c in ctx_lens)) + 16, seed=77, kv_std=1.0)
+    say("[long chunk] 1024 rows over 16k prior keys + 2 decodes, sharp")
+    got, att = _run(b)
+    assert att.info.num_prefill_items > 0
+    compare(got, oa.attention_for(b), "bf16",
+            what=f"long chunk items={att.info.num_items} tile merges={att.info.num_tile_merge_groups}")
+
+
+@pytest.mark.parametrize("kv", ["bf16"])
+def test_decodes_at_very_long_contexts(kv):
+    """Decodes over 131,072 and 131,071 keys (8192 blocks each, many split
+    spans merged inside the launch) beside a one-key decode."""
+    hq = 32
+    ctx_lens = [131072, 131071, 1]
+    b = make_batch_from_lengths("long-decodes", [1, 1, 1], ctx_lens, num_q_heads=hq, num_kv_heads=8, head_dim=128,
+                                q_dtype="bf16", kv_dtype=kv, out_dtype="bf16",
+                                n_pool_blocks=int(sum(-(-c // 16) for c in ctx_lens)) + 8, seed=78, kv_std=1.0)
+    say(f"[long decodes] kv={kv} ctx={ctx_lens}")
+    got, att = _run(b)
+    assert att.info.num_merge_groups >= 2
+    compare(got, oa.attention_for(b), "bf16", what=f"long decodes {kv} items={att.info.num_items}")
