@@ -29,7 +29,8 @@ ORDERS = {"theta": 0, "fcfs": 1, "ssjf": 2}
 
 def ablation(make_former: Callable[[dict], Callable], make_lifecycle: Callable[[], object],
              budget: int = 2048, seed: int = 0, orders=("fcfs", "ssjf", "theta"),
-             modes=(False, True), max_steps: int = 30_000, rate: float = 3.0) -> List[dict]:
+             modes=(False, True), max_steps: int = 30_000, rate: float = 3.0,
+             admit_whole_prompt: bool = False) -> List[dict]:
     """One row per (order, budget mode): the former is ``make_former(params)``
     with the sweep's former parameters for ``budget``."""
     rows = []
@@ -38,9 +39,9 @@ def ablation(make_former: Callable[[dict], Callable], make_lifecycle: Callable[[
             t0 = time.perf_counter()
             run = run_budget(budget, make_former(former_params(budget, dynamic, ORDERS[order])),
                              make_lifecycle(), seed=seed, dynamic=dynamic, max_steps=max_steps, rate=rate,
-                             max_preemptions=1_000_000)
+                             max_preemptions=1_000_000, admit_whole_prompt=admit_whole_prompt)
             m = dict(run.metrics)
-            m.update(order=order, budget_mode="dynamic" if dynamic else "static", t_max=budget, rate=rate,
+            m.update(admission="whole prompt" if admit_whole_prompt else "none", order=order, budget_mode="dynamic" if dynamic else "static", t_max=budget, rate=rate,
                      complete=run.complete, iterations=len(run.steps), sim_seconds=round(run.sim_seconds, 1),
                      wall_s=round(time.perf_counter() - t0, 2))
             rows.append(m)
@@ -52,9 +53,12 @@ def main():
     ap.add_argument("--budget", type=int, default=2048)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--rate", type=float, default=3.0, help="arrivals per second")
+    ap.add_argument("--admit-whole-prompt", action="store_true",
+                    help="offer a new request to the former only when its whole prompt fits the free blocks")
     a = ap.parse_args()
     from paper_2512_04013_amd import runtime as rt
-    for row in ablation(lambda p: rt.serving_former(**p), rt.serving_lifecycle, a.budget, a.seed, rate=a.rate):
+    for row in ablation(lambda p: rt.serving_former(**p), rt.serving_lifecycle, a.budget, a.seed, rate=a.rate,
+                        admit_whole_prompt=a.admit_whole_prompt):
         print(json.dumps(row), flush=True)
 
 

@@ -56,12 +56,13 @@ class SweepRun:
 
 def run_budget(budget: int, former: Callable, lifecycle, seed: int = 0, dynamic: bool = True,
                max_steps: int = 40_000, n_requests: int = 2000, rate: float = 3.0,
-               max_preemptions: int = 200) -> SweepRun:
+               max_preemptions: int = 200, admit_whole_prompt: bool = False) -> SweepRun:
     """Serve the seeded trace (``rate`` arrivals per second) with ``former``
     (built for this budget) and the request-record ``lifecycle`` (arrival and
     call return)."""
     trace = make_trace(n=n_requests, seed=seed, rate=rate)
-    loop = ServingLoop(trace, SimConfig(num_blocks=POOL_BLOCKS, max_preemptions=max_preemptions), lifecycle)
+    loop = ServingLoop(trace, SimConfig(num_blocks=POOL_BLOCKS, max_preemptions=max_preemptions,
+                                        admit_whole_prompt=admit_whole_prompt), lifecycle)
     try:
         loop.run(former, max_steps=max_steps)
     except RuntimeError as e:          # thrashing: the budget cannot serve the trace

@@ -89,6 +89,7 @@ class _Live:
     pause_end: float = 0.0
     parked: bool = False
     freed: bool = False
+    admitted: bool = False         # scheduled at least once
 
 
 @dataclasses.dataclass
@@ -100,6 +101,11 @@ class SimConfig:
     pred_err: float = 0.2
     max_iters: int = 10 ** 7
     max_preemptions: int = 100_000   # recompute preemptions before the loop gives up (thrashing)
+    # an engine's admission rule, not part of the paper's algorithm: a request
+    # that has never run is offered to the former only while the free blocks
+    # (less those set aside for requests admitted earlier in the same
+    # iteration) cover its whole prompt
+    admit_whole_prompt: bool = False
 
 
 @dataclasses.dataclass
@@ -198,8 +204,18 @@ class ServingLoop:
             return self.step(former)
 
         recs = self.records()
+        if self.cfg.admit_whole_prompt:
+            room, offered = self.free, []
+            for r in recs:
+                if r["state"] == WAITING and not self.live[r["id"]].admitted:
+                    need = -(-(r["ctx_len"] + r["pending"]) // BLOCK)
+                    if need > room:
+                        continue
+                    room -= need
+                offered.append(r)
+            recs = offered
         plan = former(recs, self.free, self.now)
-        order = sorted(self.live)
+        order = [r["id"] for r in recs]
         policy = {order[k]: plan["policy"][k] for k in range(len(order))}
         park_blocks = 0
         for vid in plan["park_ids"]:
@@ -229,6 +245,7 @@ class ServingLoop:
             assert self.free >= 0, "former scheduled more blocks than exist"
             r["blocks_on_gpu"] = need_total
             r["last_sched"] = self.now
+            lv.admitted = True
             r["state"] = RUNNING
             if r["pending"] > 0:
                 r["ctx_len"] += t

@@ -69,6 +69,34 @@ def test_paused_requests_are_never_scheduled():
     assert len(loop.done) == len(trace)
 
 
+def test_whole_prompt_admission_offers_only_new_requests_that_fit():
+    """With the admission rule on, every never-run request offered to the
+    former has its whole prompt covered by the free blocks, after those of
+    the new requests offered before it; the trace still completes, in lock
+    step between the two formers."""
+    from synth.trace import BLOCK, WAITING
+    trace = small_trace(seed=11)
+    p = params_for(1024, True)
+    both = lockstep(oracle_former(p), library_former(p))
+    loop = ServingLoop(trace, SimConfig(num_blocks=384, admit_whole_prompt=True), LockstepLifecycle())
+    held_back = []
+
+    def checked(recs, free, now):
+        room = free
+        offered = {r["id"] for r in recs}
+        for r in recs:
+            if r["state"] == WAITING and not loop.live[r["id"]].admitted:
+                need = -(-(r["ctx_len"] + r["pending"]) // BLOCK)
+                assert need <= room
+                room -= need
+        held_back.append(len(loop.live) - len(offered))
+        return both(recs, free, now)
+
+    loop.run(checked)
+    assert len(loop.done) == len(trace)
+    assert max(held_back) > 0          # the rule did hold requests back
+
+
 def test_a_pool_far_too_small_is_reported_not_looped_on():
     trace = small_trace(seed=256)
     loop = ServingLoop(trace, SimConfig(num_blocks=48, max_preemptions=200), OracleLifecycle())
