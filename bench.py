@@ -227,6 +227,46 @@ def park_resume_rates(b, kv, log, reps: int = 3):
     return r
 
 
+class TimingEvent:
+    """A HIP timing event created with hipEventDisableSystemFence: its
+    timestamp is taken when the stream reaches it, without the system-scope
+    cache write-back and invalidation of an ordinary event, which would
+    otherwise fall inside the measured window and delay the next launch (the
+    HIP runtime documents the flag for timing-only events). Same record /
+    elapsed_time interface as torch.cuda.Event."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+    _hip = None
+
+    def __init__(self):
+        import ctypes as C
+        if TimingEvent._hip is None:
+            # the HIP runtime torch has already loaded, so that its streams are valid here
+            loaded = sorted({ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64" in ln})
+            L = C.CDLL(loaded[0] if loaded else "libamdhip64.so.7")
+            L.hipEventCreateWithFlags.argtypes = [C.POINTER(C.c_void_p), C.c_uint]
+            L.hipEventRecord.argtypes = [C.c_void_p, C.c_void_p]
+            L.hipEventSynchronize.argtypes = [C.c_void_p]
+            L.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+            TimingEvent._hip = L
+        self._c = C
+        self.h = C.c_void_p()
+        if self._hip.hipEventCreateWithFlags(C.byref(self.h), self.DISABLE_SYSTEM_FENCE) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self, stream):
+        if self._hip.hipEventRecord(self.h, self._c.c_void_p(stream.cuda_stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, end: "TimingEvent") -> float:
+        """Milliseconds from this event to ``end`` (waits for ``end``)."""
+        ms = self._c.c_float()
+        if self._hip.hipEventSynchronize(end.h) != 0 or \
+                self._hip.hipEventElapsedTime(self._c.byref(ms), self.h, end.h) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+
 def time_layers(n_layers, shape, info, plan_dev, k_new, v_new, q, pools, bids, num_pool_blocks, out, ws,
                 stream, log, reps: int = 20):
     """One planned batch run as ``n_layers`` layers (per layer: the KV append
@@ -383,7 +423,7 @@ def budget_sweep(args, log):
             bid_dev = up_dev[off:off + bids.nbytes].view(torch.int32)
             host_ev[slot] = torch.cuda.Event()
             host_ev[slot].record(stream)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0, e1 = TimingEvent(), TimingEvent()
             e0.record(stream)
             aug.aug_attn_mixed(shape, info, plan_dev, q, k_cache, v_cache, k_scale, v_scale, bid_dev, nb, out,
                                ws_dev, stream=stream.cuda_stream)
@@ -542,9 +582,7 @@ def main():
         aug.aug_plan_upload(host, plan_dev, plan.size, stream=stream.cuda_stream)
         plan_ev[slot] = torch.cuda.Event()
         plan_ev[slot].record(stream)
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        a0 = torch.cuda.Event(enable_timing=True)
+        e0, e1, a0 = TimingEvent(), TimingEvent(), TimingEvent()
         kc, vc, ksc, vsc = pools[i % len(pools)]
         a0.record(stream)
         aug.aug_kv_append(shape, info, plan_dev, k_new, v_new, kc, vc, ksc, vsc, bids, kv.num_pool_blocks,
