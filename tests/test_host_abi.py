@@ -231,17 +231,24 @@ def test_planning_from_several_threads_gives_the_serial_plans():
     """The binding releases the GIL inside the planner; plans made on eight
     threads at once must equal the plans made one after another."""
     import threading
-    batches = [synth.make_tiny_mixed(seed=s) for s in range(4)] + \
-              [synth.make_mixed_8b(seed=s, n_dec=48, n_pre=2, n_pool_blocks=16384) for s in range(4)]
-    want = [aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks, b.block_ids)[1]
-            for b in batches]
+    shape = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)
+    batches = []
+    for k in range(8):                  # batch descriptions only: the planner reads no KV
+        rng = np.random.default_rng(k)
+        n = 64 + 32 * k
+        q = np.where(rng.random(n) < 0.1, rng.integers(2, 300, n), 1)
+        ctx = q + rng.integers(0, 3000, n)
+        nblk = (ctx + 15) // 16
+        q_start = np.concatenate([[0], np.cumsum(q)])
+        bt_start = np.concatenate([[0], np.cumsum(nblk)])
+        pool = int(bt_start[-1]) + 16
+        batches.append((q_start, ctx, bt_start, pool, rng.permutation(pool)[:bt_start[-1]]))
+    want = [aug.aug_attn_plan(shape, *b)[1] for b in batches]
     bad = []
 
     def worker(k):
-        b = batches[k]
         for _ in range(30):
-            _, plan = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
-                                        b.block_ids)
+            _, plan = aug.aug_attn_plan(shape, *batches[k])
             if not np.array_equal(plan, want[k]):
                 bad.append(k)
 
