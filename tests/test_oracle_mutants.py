@@ -14,6 +14,7 @@ import pytest
 from oracle import attention as oa
 from oracle import former as of
 from oracle import kvappend as ka
+from oracle import kvpark as kp
 from oracle.codecs import E4M3FN_TABLE, bf16_bits_to_f64, e4m3fn_encode
 from tests import test_oracle_append as pins_append
 from tests import test_oracle_attention as pins_attention
@@ -165,6 +166,47 @@ def test_append_pins_catch(mutant, monkeypatch):
     monkeypatch.setattr(ka, name, fn)
     fails, runs = _run_pins(pins_append)
     assert fails > 0, f"{mutant}: none of {runs} append pins failed"
+
+
+# ---- park / resume -----------------------------------------------------------------------
+
+def _park(v_first=False, no_scales=False, k_scale_twice=False, sort_blocks=False):
+    def park(k_cache, v_cache, k_scale, v_scale, kv_dtype, blocks):
+        parts = []
+        blocks = np.asarray(blocks, dtype=np.int64)
+        for b in (np.sort(blocks) if sort_blocks else blocks):
+            kb = np.ascontiguousarray(k_cache[b]).view(np.uint8).ravel()
+            vb = np.ascontiguousarray(v_cache[b]).view(np.uint8).ravel()
+            parts += [vb, kb] if v_first else [kb, vb]
+            if kv_dtype == "fp8" and not no_scales:
+                parts.append(np.ascontiguousarray(k_scale[b], dtype=np.float32).view(np.uint8).ravel())
+                second = k_scale if k_scale_twice else v_scale
+                parts.append(np.ascontiguousarray(second[b], dtype=np.float32).view(np.uint8).ravel())
+        return np.concatenate(parts) if parts else np.zeros(0, np.uint8)
+    return park
+
+
+def _resume_reversed(k_cache, v_cache, k_scale, v_scale, kv_dtype, blocks, image):
+    return _ORIGINAL_RESUME(k_cache, v_cache, k_scale, v_scale, kv_dtype, np.asarray(blocks)[::-1], image)
+
+
+_ORIGINAL_RESUME = kp.resume
+
+PARK_MUTANTS = {
+    "V before K in a record": ("park", _park(v_first=True)),
+    "fp8 scales left out of the record": ("park", _park(no_scales=True)),
+    "K scale written in place of the V scale": ("park", _park(k_scale_twice=True)),
+    "blocks parked in sorted order, not the listed one": ("park", _park(sort_blocks=True)),
+    "records resumed into the blocks in reverse": ("resume", _resume_reversed),
+}
+
+
+@pytest.mark.parametrize("mutant", sorted(PARK_MUTANTS))
+def test_park_pins_catch(mutant, monkeypatch):
+    name, fn = PARK_MUTANTS[mutant]
+    monkeypatch.setattr(kp, name, fn)
+    fails, runs = _run_pins(pins_attention)
+    assert fails > 0, f"{mutant}: none of {runs} attention and park pins failed"
 
 
 # ---- batch former ------------------------------------------------------------------------
