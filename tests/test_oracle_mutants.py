@@ -15,6 +15,7 @@ from oracle import attention as oa
 from oracle import former as of
 from oracle import kvappend as ka
 from oracle import kvpark as kp
+from oracle import codecs as oc
 from oracle.codecs import E4M3FN_TABLE, bf16_bits_to_f64, e4m3fn_encode
 from tests import test_oracle_append as pins_append
 from tests import test_oracle_attention as pins_attention
@@ -166,6 +167,46 @@ def test_append_pins_catch(mutant, monkeypatch):
     monkeypatch.setattr(ka, name, fn)
     fails, runs = _run_pins(pins_append)
     assert fails > 0, f"{mutant}: none of {runs} append pins failed"
+
+
+# ---- number formats ----------------------------------------------------------------------
+
+def _e4m3(bias=7, subnormal_as_normal=False, nan_only_all_ones=False):
+    def value(code):
+        code = int(code) & 0xFF
+        sign = -1.0 if code & 0x80 else 1.0
+        e, m = (code >> 3) & 0xF, code & 0x7
+        if (code & 0x7F) == 0x7F and not nan_only_all_ones or code == 0xFF and nan_only_all_ones:
+            return float("nan")
+        if e == 0 and not subnormal_as_normal:
+            return sign * m * 2.0 ** -9
+        return sign * (1.0 + m / 8.0) * 2.0 ** (e - bias)
+    return value
+
+
+FORMAT_MUTANTS = {
+    "E4M3FN exponent bias 8": _e4m3(bias=8),
+    "E4M3FN subnormals read as normals": _e4m3(subnormal_as_normal=True),
+    "E4M3FN NaN only at 0xFF": _e4m3(nan_only_all_ones=True),
+}
+
+
+@pytest.mark.parametrize("mutant", sorted(FORMAT_MUTANTS))
+def test_format_pins_catch(mutant, monkeypatch):
+    fn = FORMAT_MUTANTS[mutant]
+    monkeypatch.setattr(oc, "e4m3fn_value", fn)
+    monkeypatch.setattr(oc, "E4M3FN_TABLE", np.array([fn(c) for c in range(256)], dtype=np.float64))
+    fails, runs = _run_pins(pins_attention)
+    assert fails > 0, f"{mutant}: none of {runs} attention pins failed"
+
+
+def test_bf16_decoder_mutant_is_caught(monkeypatch):
+    def shifted(u16):   # bf16 bits placed one position too low in the float32
+        u32 = np.asarray(u16, dtype=np.uint16).astype(np.uint32) << np.uint32(15)
+        return u32.view(np.float32).astype(np.float64)
+    monkeypatch.setattr(oc, "bf16_bits_to_f64", shifted)
+    fails, runs = _run_pins(pins_attention)
+    assert fails > 0, f"bf16 decoder shifted: none of {runs} attention pins failed"
 
 
 # ---- park / resume -----------------------------------------------------------------------
