@@ -134,6 +134,15 @@ typedef struct {
   int32_t num_reqs;
   int32_t num_tile_merge_groups;
   int32_t num_append_items;  /* blocks that receive new K/V rows (aug_kv_append) */
+  /* The layer shape the plan was built for. aug_attn_mixed and aug_kv_append
+   * refuse a call whose shape differs in any of these fields: the plan's work
+   * items, partial sizes and workspace size depend on them. */
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t q_dtype;
+  int32_t kv_dtype;
+  int32_t out_dtype;
   int32_t reserved;
 } aug_attn_plan_info;
 
@@ -142,18 +151,28 @@ typedef struct {
  * plan_host == NULL to obtain the sizes only). The image is position
  * independent: copy it verbatim to device memory and pass that copy to
  * aug_attn_mixed with the same `info`. kv_split_tokens <= 0 lets the planner
- * choose the decode split (keys per work item); a positive value is rounded
- * up to a multiple of block_size. Pure host code; deterministic.
+ * choose the decode split (keys per work item); a positive value, at most
+ * 2^24, is rounded up to a multiple of block_size. Contexts are limited to
+ * 2^24 tokens per request. Pure host code; deterministic.
  * The image also lists the blocks that receive the step's new K/V rows
  * (info->num_append_items), for aug_kv_append.
  * Errors: AUG_ERR_INVALID (shape, monotonicity, ctx_len < q_len, too few
- * blocks, block id outside the pool; with the host block table, a block that
- * would receive new tokens of two requests or twice from one),
- * AUG_ERR_UNSUPPORTED (dtype set, head_dim, block_size), AUG_ERR_NO_SPACE
- * (plan_cap < plan_bytes). */
+ * blocks, block id outside the pool, kv_split_tokens above 2^24; with the
+ * host block table, a block that would receive new tokens of two requests or
+ * twice from one), AUG_ERR_UNSUPPORTED (dtype set, head_dim, block_size, a
+ * context above 2^24 tokens), AUG_ERR_NO_SPACE (plan_cap < plan_bytes). */
 aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batch,
                          int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
                          aug_attn_plan_info* info);
+
+/* Device workspace (split-K partials, in bytes) that aug_attn_mixed needs for
+ * this batch with this split: the planner's size query, the same validation
+ * as aug_attn_plan, nothing written but *bytes. The batch is the formed batch
+ * of the problem statement (requests with their query rows, context lengths
+ * and block tables); the size depends on the split the planner chooses.
+ * Errors: those of aug_attn_plan; AUG_ERR_INVALID for a NULL `bytes`. */
+aug_status aug_attn_workspace_size(const aug_attn_shape* shape, const aug_batch_desc* batch,
+                                   int32_t kv_split_tokens, size_t* bytes);
 
 /* Copy `bytes` bytes of a plan image (or any other bytes) from pinned host
  * memory host_src to device memory dev_dst with one small copy kernel
@@ -191,7 +210,8 @@ aug_status aug_plan_upload(const void* host_src, void* dev_dst, size_t bytes, vo
  * split decode rows are merged in it by the workgroup that finishes each
  * row's last span; split prefill tiles are merged by a second small launch
  * when info->num_tile_merge_groups > 0.
- * Errors: AUG_ERR_INVALID (NULL pointers, info/shape mismatch),
+ * Errors: AUG_ERR_INVALID (NULL pointers, info inconsistent, or a shape
+ * other than the one the plan was built for: heads, head_dim or dtypes),
  * AUG_ERR_NO_SPACE (workspace_bytes too small), AUG_ERR_HIP (launch). */
 aug_status aug_attn_mixed(const aug_attn_shape* shape, const aug_attn_plan_info* info,
                           void* plan_dev, const void* q, const void* k_cache,
@@ -224,8 +244,8 @@ aug_status aug_attn_mixed(const aug_attn_shape* shape, const aug_attn_plan_info*
  * race on its contents and scale. Enqueued on `stream` as one kernel launch
  * (none for an empty batch); no allocation, no memset, so the call can be
  * captured in a HIP graph and replayed.
- * Errors: AUG_ERR_INVALID (NULL pointers, info/shape mismatch,
- * missing scales for fp8), AUG_ERR_HIP (launch). */
+ * Errors: AUG_ERR_INVALID (NULL pointers, info inconsistent or built for
+ * another shape, missing scales for fp8), AUG_ERR_HIP (launch). */
 aug_status aug_kv_append(const aug_attn_shape* shape, const aug_attn_plan_info* info,
                          const void* plan_dev, const void* k_new, const void* v_new, void* k_cache,
                          void* v_cache, float* k_scale, float* v_scale, const int32_t* block_ids,
@@ -248,10 +268,13 @@ size_t aug_kv_record_bytes(const aug_attn_shape* shape);
  * larger copies): a gather kernel fills it, then an asynchronous copy drains
  * it to host_dst, chunk after chunk, all on `stream`. host_dst is complete
  * once the stream reaches the end of this call's work.
- * block_ids_dev: device int32[n_blocks]. block_ids_host: optional host copy,
- * range-checked against num_pool_blocks when given; the kernel itself skips
- * (and leaves undefined) any record whose id is outside the pool.
- * Errors: AUG_ERR_INVALID, AUG_ERR_NO_SPACE (host_bytes, staging_bytes),
+ * block_ids_dev: device int32[n_blocks]. block_ids_host: the same ids in
+ * host memory (required), range-checked against num_pool_blocks before
+ * anything is enqueued, so every record of a successful call is the block's
+ * bytes. (Should the device copy still name a block outside the pool, the
+ * kernel never dereferences it and writes a record of zero bytes instead.)
+ * Errors: AUG_ERR_INVALID (NULL pointers, block_ids_host missing, an id
+ * outside the pool), AUG_ERR_NO_SPACE (host_bytes, staging_bytes),
  * AUG_ERR_HIP. */
 aug_status aug_kv_park(const aug_attn_shape* shape, const void* k_cache, const void* v_cache,
                        const float* k_scale, const float* v_scale,
@@ -262,7 +285,8 @@ aug_status aug_kv_park(const aug_attn_shape* shape, const void* k_cache, const v
 /* Resume n_blocks records from host_src (pinned, as written by aug_kv_park)
  * into the pool blocks block_ids_dev[0..n_blocks-1] (any blocks: a resumed
  * request usually lands elsewhere than it was). Same staging scheme in the
- * other direction. Ids outside the pool are skipped by the kernel.
+ * other direction; block_ids_host is required and range-checked as for
+ * aug_kv_park (a device id outside the pool is never written).
  * Errors as aug_kv_park. */
 aug_status aug_kv_resume(const aug_attn_shape* shape, void* k_cache, void* v_cache,
                          float* k_scale, float* v_scale, const int32_t* block_ids_dev,

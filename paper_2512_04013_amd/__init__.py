@@ -23,6 +23,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libaug.so")
+# Test runs of the host code under the sanitizers load a host-only build of
+# the planner and former instead (no device entry points: calling one raises).
+_HOST_ONLY_LIB = os.environ.get("AUG_HOST_ONLY_LIB")
 
 AUG_OK, AUG_ERR_INVALID, AUG_ERR_UNSUPPORTED, AUG_ERR_NO_SPACE, AUG_ERR_HIP = 0, -1, -2, -3, -4
 AUG_F32, AUG_BF16, AUG_FP8_E4M3FN = 0, 1, 2
@@ -31,7 +34,8 @@ AUG_POL_NONE, AUG_PRESERVE, AUG_DISCARD, AUG_SWAP = 0, 1, 2, 3
 
 DTYPE_CODES = {"f32": AUG_F32, "bf16": AUG_BF16, "fp8": AUG_FP8_E4M3FN}
 
-EXPORTED = ["aug_request_arrive", "aug_request_return", "aug_attn_plan", "aug_plan_upload", "aug_attn_mixed",
+EXPORTED = ["aug_request_arrive", "aug_request_return", "aug_attn_plan", "aug_attn_workspace_size",
+            "aug_plan_upload", "aug_attn_mixed",
             "aug_kv_append", "aug_kv_record_bytes", "aug_kv_park", "aug_kv_resume", "aug_form_batch",
             "aug_status_string", "aug_last_error", "aug_abi_version"]
 
@@ -62,6 +66,8 @@ class aug_attn_plan_info(C.Structure):
                 ("num_partials", C.c_int32), ("kv_split_tokens", C.c_int32),
                 ("total_rows", C.c_int32), ("num_reqs", C.c_int32),
                 ("num_tile_merge_groups", C.c_int32), ("num_append_items", C.c_int32),
+                ("num_q_heads", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("q_dtype", C.c_int32), ("kv_dtype", C.c_int32), ("out_dtype", C.c_int32),
                 ("reserved", C.c_int32)]
 
 
@@ -109,13 +115,18 @@ def lib():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(LIB_PATH):
-        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+    path = _HOST_ONLY_LIB or LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with "
                            "`python -m paper_2512_04013_amd.build` (or __graft_entry__.build())")
-    L = C.CDLL(LIB_PATH)
+    L = C.CDLL(path)
+    if _HOST_ONLY_LIB:
+        L = _HostOnly(L)
     P = C.c_void_p
     L.aug_attn_plan.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_batch_desc), C.c_int32, P,
                                 C.c_size_t, C.POINTER(aug_attn_plan_info)]
+    L.aug_attn_workspace_size.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_batch_desc), C.c_int32,
+                                          C.POINTER(C.c_size_t)]
     L.aug_attn_mixed.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P,
                                  P, P, P, C.c_int32, P, P, C.c_size_t, P]
     L.aug_kv_append.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P, P,
@@ -131,7 +142,7 @@ def lib():
                                  C.POINTER(aug_batch_plan)]
     L.aug_request_arrive.argtypes = [P, C.c_int64, C.c_double, C.c_int32, C.c_int32, C.c_double, C.c_int32]
     L.aug_request_return.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_double, C.c_int32]
-    for f in ("aug_attn_plan", "aug_plan_upload", "aug_attn_mixed", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
+    for f in ("aug_attn_plan", "aug_attn_workspace_size", "aug_plan_upload", "aug_attn_mixed", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
               "aug_form_batch", "aug_request_arrive", "aug_request_return"):
         getattr(L, f).restype = C.c_int
     L.aug_status_string.argtypes = [C.c_int]
@@ -141,6 +152,24 @@ def lib():
     L.aug_abi_version.restype = C.c_int32
     _lib = L
     return L
+
+
+class _HostOnly:
+    """A host-only build: its functions, and for each device entry point it
+    lacks a stand-in that raises when called."""
+
+    def __init__(self, L):
+        self._L = L
+
+    def __getattr__(self, name):
+        try:
+            return getattr(self._L, name)
+        except AttributeError:
+            def missing(*a, **k):
+                raise RuntimeError(f"{name} is not in the host-only library {_HOST_ONLY_LIB}")
+            missing.argtypes = missing.restype = None
+            setattr(self, name, missing)
+            return missing
 
 
 def aug_status_string(status: int) -> str:
@@ -199,17 +228,24 @@ def make_shape(num_q_heads, num_kv_heads, head_dim, q_dtype, kv_dtype, out_dtype
                           code(kv_dtype), code(out_dtype), softmax_scale)
 
 
-def aug_attn_plan(shape: aug_attn_shape, q_start, ctx_len, bt_start, num_pool_blocks: int,
-                  block_ids=None, kv_split_tokens: int = 0):
-    """Validate a batch (host arrays) and build its plan image.
-    Returns (info, plan) with plan a numpy uint8 array of info.plan_bytes bytes."""
-    L = lib()
+def _batch_desc(q_start, ctx_len, bt_start, num_pool_blocks, block_ids=None):
+    """The C batch description and the int32 arrays it points into (which the
+    caller keeps alive for the call)."""
     qs, cl, bs = _i32(q_start), _i32(ctx_len), _i32(bt_start)
     bi = None if block_ids is None else _i32(block_ids)
     p32 = C.POINTER(C.c_int32)
     desc = aug_batch_desc(len(cl), qs.ctypes.data_as(p32), cl.ctypes.data_as(p32),
                           bs.ctypes.data_as(p32), None if bi is None else bi.ctypes.data_as(p32),
                           int(num_pool_blocks))
+    return desc, (qs, cl, bs, bi)
+
+
+def aug_attn_plan(shape: aug_attn_shape, q_start, ctx_len, bt_start, num_pool_blocks: int,
+                  block_ids=None, kv_split_tokens: int = 0):
+    """Validate a batch (host arrays) and build its plan image.
+    Returns (info, plan) with plan a numpy uint8 array of info.plan_bytes bytes."""
+    L = lib()
+    desc, keep = _batch_desc(q_start, ctx_len, bt_start, num_pool_blocks, block_ids)
     info = aug_attn_plan_info()
     # one scratch image per thread: ctypes releases the GIL during the call
     buf = getattr(_plan_scratch, "buf", None)
@@ -226,6 +262,17 @@ def aug_attn_plan(shape: aug_attn_shape, q_start, ctx_len, bt_start, num_pool_bl
 
 
 _plan_scratch = threading.local()
+
+
+def aug_attn_workspace_size(shape: aug_attn_shape, q_start, ctx_len, bt_start, num_pool_blocks: int,
+                            block_ids=None, kv_split_tokens: int = 0) -> int:
+    """Bytes of device workspace aug_attn_mixed needs for this batch and split."""
+    desc, keep = _batch_desc(q_start, ctx_len, bt_start, num_pool_blocks, block_ids)
+    n = C.c_size_t(0)
+    _check(lib().aug_attn_workspace_size(C.byref(shape), C.byref(desc), int(kv_split_tokens), C.byref(n)),
+           "aug_attn_workspace_size")
+    del keep
+    return int(n.value)
 
 
 def aug_plan_upload(host_src, dev_dst, nbytes: Optional[int] = None, stream=None):

@@ -69,5 +69,29 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+HOST_SAN_LIB = os.path.join(BUILD, "libaug_host_san.so")
+
+
+def build_host_sanitized(verbose: bool = False) -> str:
+    """The host-only sources (planner, batch former, status strings) built by
+    g++ with AddressSanitizer and UndefinedBehaviorSanitizer into
+    ``_build/libaug_host_san.so``, for CPU test runs of the host code under the
+    sanitizers (the process must preload the compiler's libasan). The library
+    has no device entry points."""
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = [os.path.join(CSRC, s) for s in CPP_SOURCES]
+    tmp = HOST_SAN_LIB + ".tmp"
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-shared", f"-I{INCLUDE}", f"-I{CSRC}",
+           "-ffp-contract=off", "-fno-fast-math", "-fno-omit-frame-pointer",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=all", *srcs, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized host build failed:\n{r.stdout}{r.stderr}")
+    os.replace(tmp, HOST_SAN_LIB)
+    return HOST_SAN_LIB
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

@@ -45,12 +45,9 @@
 #include <type_traits>
 
 #include "aug.h"
+#include "checks.h"
 #include "plan_format.h"
 #include "status.h"
-
-namespace aug {
-aug_status check_shape(const aug_attn_shape* s, const char* who);
-}
 
 namespace {
 
@@ -1340,12 +1337,7 @@ extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_pla
                                      void* workspace, size_t workspace_bytes, void* stream) {
   const char* who = "aug_attn_mixed";
   if (aug_status st = aug::check_shape(s, who); st != AUG_OK) return st;
-  if (!info) return aug::fail(AUG_ERR_INVALID, "%s: info is NULL", who);
-  if (info->num_items < 0 || info->num_merge_groups < 0 || info->num_partials < 0 ||
-      info->num_tile_merge_groups < 0 || info->num_tile_merge_groups > info->num_merge_groups ||
-      info->num_append_items < 0 ||
-      info->plan_bytes != aug::plan_image_bytes(info->num_items, info->num_merge_groups, info->num_append_items))
-    return aug::fail(AUG_ERR_INVALID, "%s: info is inconsistent", who);
+  if (aug_status st = aug::check_plan_info(info, s, who); st != AUG_OK) return st;
   if (info->num_items == 0) return AUG_OK;
   if (!plan_dev || !q || !k_cache || !v_cache || !block_ids || !out)
     return aug::fail(AUG_ERR_INVALID, "%s: NULL device pointer", who);

@@ -20,12 +20,10 @@
 #include <cstdint>
 
 #include "aug.h"
+#include "checks.h"
 #include "plan_format.h"
 #include "status.h"
 
-namespace aug {
-aug_status check_shape(const aug_attn_shape* s, const char* who);
-}
 
 namespace {
 
@@ -194,12 +192,8 @@ extern "C" aug_status aug_kv_append(const aug_attn_shape* s, const aug_attn_plan
                                     const int32_t* block_ids, int32_t num_pool_blocks, void* stream) {
   const char* who = "aug_kv_append";
   if (aug_status st = aug::check_shape(s, who); st != AUG_OK) return st;
-  if (!info) return aug::fail(AUG_ERR_INVALID, "%s: info is NULL", who);
-  if (info->num_append_items < 0 || info->num_items < 0 || info->num_merge_groups < 0)
-    return aug::fail(AUG_ERR_INVALID, "%s: info is not a plan's", who);
+  if (aug_status st = aug::check_plan_info(info, s, who); st != AUG_OK) return st;
   const int64_t append_off = aug::append_offset(info->num_items, info->num_merge_groups);
-  if (aug::plan_image_bytes(info->num_items, info->num_merge_groups, info->num_append_items) != info->plan_bytes)
-    return aug::fail(AUG_ERR_INVALID, "%s: info does not describe a plan image of this layout", who);
   if (info->num_append_items == 0) return AUG_OK;
   if (!plan_dev || !k_new || !v_new || !k_cache || !v_cache || !block_ids)
     return aug::fail(AUG_ERR_INVALID, "%s: NULL device pointer", who);

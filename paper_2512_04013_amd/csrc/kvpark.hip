@@ -19,11 +19,8 @@
 #include <cstdint>
 
 #include "aug.h"
+#include "checks.h"
 #include "status.h"
-
-namespace aug {
-aug_status check_shape(const aug_attn_shape* s, const char* who);
-}
 
 namespace {
 
@@ -61,12 +58,22 @@ __device__ __forceinline__ void wg_copy(char* dst, const char* src, int64_t byte
   }
 }
 
+// Zero `bytes` (a multiple of 4) cooperatively across the workgroup.
+__device__ __forceinline__ void wg_zero(char* dst, int64_t bytes) {
+  uint32_t* d = reinterpret_cast<uint32_t*>(dst);
+  for (int64_t i = threadIdx.x; i < bytes / 4; i += kThreads) d[i] = 0u;
+}
+
 __global__ __launch_bounds__(kThreads) void gather_kernel(
     const char* k_cache, const char* v_cache, const char* k_scale, const char* v_scale,
     const int32_t* ids, int32_t first, int32_t num_pool_blocks, RecordGeom g, char* staging) {
   const int32_t bid = ids[first + blockIdx.x];
-  if (static_cast<uint32_t>(bid) >= static_cast<uint32_t>(num_pool_blocks)) return;
   char* rec = staging + static_cast<int64_t>(blockIdx.x) * g.rec_bytes;
+  if (static_cast<uint32_t>(bid) >= static_cast<uint32_t>(num_pool_blocks)) {
+    // never dereferenced; the record reads as zero bytes rather than stale staging
+    wg_zero(rec, g.rec_bytes);
+    return;
+  }
   wg_copy(rec, k_cache + static_cast<int64_t>(bid) * g.kv_bytes, g.kv_bytes);
   wg_copy(rec + g.kv_bytes, v_cache + static_cast<int64_t>(bid) * g.kv_bytes, g.kv_bytes);
   if (g.scale_bytes) {
@@ -111,7 +118,8 @@ aug_status check_common(const char* who, const aug_attn_shape* s, const void* k,
   if (staging_bytes < static_cast<size_t>(g->rec_bytes))
     return aug::fail(AUG_ERR_NO_SPACE, "%s: staging %zu < one record (%lld bytes)", who,
                      staging_bytes, (long long)g->rec_bytes);
-  if (ids_host) {
+  if (!ids_host) return aug::fail(AUG_ERR_INVALID, "%s: block_ids_host is required", who);
+  {
     for (int32_t i = 0; i < n_blocks; ++i)
       if (ids_host[i] < 0 || ids_host[i] >= num_pool_blocks)
         return aug::fail(AUG_ERR_INVALID, "%s: block id %d (entry %d) outside a pool of %d", who,

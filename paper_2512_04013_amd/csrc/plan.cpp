@@ -19,6 +19,7 @@
 #include <vector>
 
 #include "aug.h"
+#include "checks.h"
 #include "plan_format.h"
 #include "status.h"
 
@@ -40,6 +41,8 @@ aug_status check_shape(const aug_attn_shape* s, const char* who) {
   if (s->num_q_heads < 1 || s->num_kv_heads < 1 || s->num_q_heads % s->num_kv_heads != 0)
     return fail(AUG_ERR_INVALID, "%s: heads %d/%d are not a positive multiple", who,
                 s->num_q_heads, s->num_kv_heads);
+  if (s->num_kv_heads > 1024)
+    return fail(AUG_ERR_UNSUPPORTED, "%s: %d KV heads (supported: up to 1024)", who, s->num_kv_heads);
   const int g = s->num_q_heads / s->num_kv_heads;
   if (g != 1 && g != 2 && g != 4 && g != 8)
     return fail(AUG_ERR_UNSUPPORTED, "%s: group size %d (supported: 1, 2, 4, 8)", who, g);
@@ -54,6 +57,26 @@ aug_status check_shape(const aug_attn_shape* s, const char* who) {
     return fail(AUG_ERR_UNSUPPORTED, "%s: fp8 KV needs head_dim 128", who);
   if (!std::isfinite(s->softmax_scale) || !(s->softmax_scale > 0.f))
     return fail(AUG_ERR_INVALID, "%s: softmax_scale must be finite and positive", who);
+  return AUG_OK;
+}
+
+aug_status check_plan_info(const aug_attn_plan_info* info, const aug_attn_shape* s, const char* who) {
+  if (!info) return fail(AUG_ERR_INVALID, "%s: info is NULL", who);
+  if (info->num_items < 0 || info->num_merge_groups < 0 || info->num_partials < 0 ||
+      info->num_tile_merge_groups < 0 || info->num_tile_merge_groups > info->num_merge_groups ||
+      info->num_append_items < 0 || info->num_prefill_items < 0 || info->num_prefill_items > info->num_items ||
+      info->workspace_bytes < 0 ||
+      info->plan_bytes != plan_image_bytes(info->num_items, info->num_merge_groups, info->num_append_items))
+    return fail(AUG_ERR_INVALID, "%s: info is not consistent with a plan image", who);
+  if (info->num_q_heads != s->num_q_heads || info->num_kv_heads != s->num_kv_heads ||
+      info->head_dim != s->head_dim || info->q_dtype != s->q_dtype || info->kv_dtype != s->kv_dtype ||
+      info->out_dtype != s->out_dtype)
+    return fail(AUG_ERR_INVALID,
+                "%s: the plan was built for heads %d/%d, head_dim %d, dtypes %d/%d/%d; called with "
+                "%d/%d, %d, %d/%d/%d",
+                who, info->num_q_heads, info->num_kv_heads, info->head_dim, info->q_dtype, info->kv_dtype,
+                info->out_dtype, s->num_q_heads, s->num_kv_heads, s->head_dim, s->q_dtype, s->kv_dtype,
+                s->out_dtype);
   return AUG_OK;
 }
 
@@ -87,7 +110,7 @@ double merge_ns(int64_t partial_bytes) {
 double makespan_bound(double longest, double total) { return std::max(longest, total / kSlots); }
 
 int32_t choose_split(int64_t total_row_keys, int32_t requested) {
-  if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;
+  if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;   // requested <= kMaxSplit
   // About four row items per compute unit (256 CUs), but never spans under
   // 512 keys (on small batches an item's fixed latency, query load, state
   // merge and partial write, outweighs shorter streams); on large batches
@@ -115,6 +138,8 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   if (n > 0 && (!b->q_start || !b->ctx_len || !b->bt_start))
     return fail(AUG_ERR_INVALID, "%s: batch arrays are NULL", who);
   if (b->num_pool_blocks < 1) return fail(AUG_ERR_INVALID, "%s: empty pool", who);
+  if (kv_split_tokens > kMaxSplit)
+    return fail(AUG_ERR_INVALID, "%s: kv_split_tokens %d > %d", who, kv_split_tokens, kMaxSplit);
   if (n > 0 && b->q_start[0] != 0) return fail(AUG_ERR_INVALID, "%s: q_start[0] != 0", who);
   const int32_t hkv = s->num_kv_heads;
   const int32_t g = s->num_q_heads / hkv;
@@ -126,6 +151,9 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
     if (ctx < q)
       return fail(AUG_ERR_INVALID, "%s: request %d has ctx_len %lld < rows %lld", who, r,
                   (long long)ctx, (long long)q);
+    if (ctx > kMaxContext)
+      return fail(AUG_ERR_UNSUPPORTED, "%s: request %d has ctx_len %lld > %d", who, r, (long long)ctx,
+                  kMaxContext);
     const int64_t need = (ctx + kBlock - 1) / kBlock;
     const int64_t have = static_cast<int64_t>(b->bt_start[r + 1]) - b->bt_start[r];
     if (b->bt_start[r] < 0 || have < need)
@@ -202,6 +230,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
     bool have = false;
     for (const int32_t cand : {kTileSpanMax, 4096, 2048, 1024, 512, kTileSpanMin}) {
       if (have && longest_tile <= cand) continue;   // nothing splits: same as the longer span
+      if (have && longest_tile / cand > 1024) continue;   // at most ~1k spans per tile row
       double total = row_total, longest = row_longest;
       int64_t partial_bytes = row_partial_bytes;
       for (int32_t r = 0; r < n; ++r) {
@@ -337,6 +366,12 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   info->num_reqs = n;
   info->num_tile_merge_groups = static_cast<int32_t>(tile_groups.size());
   info->num_append_items = static_cast<int32_t>(n_append);
+  info->num_q_heads = s->num_q_heads;
+  info->num_kv_heads = hkv;
+  info->head_dim = s->head_dim;
+  info->q_dtype = s->q_dtype;
+  info->kv_dtype = s->kv_dtype;
+  info->out_dtype = s->out_dtype;
   if (!plan_host) return AUG_OK;
   if (plan_cap < static_cast<size_t>(plan_bytes))
     return fail(AUG_ERR_NO_SPACE, "%s: plan buffer %zu < %lld bytes", who, plan_cap,
@@ -357,6 +392,12 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   hdr.counters_offset = static_cast<int32_t>(counters_off);
   hdr.append_offset = static_cast<int32_t>(append_off);
   hdr.num_append_items = static_cast<int32_t>(n_append);
+  hdr.num_q_heads = static_cast<int16_t>(s->num_q_heads);
+  hdr.num_kv_heads = static_cast<int16_t>(hkv);
+  hdr.head_dim = static_cast<int16_t>(s->head_dim);
+  hdr.q_dtype = static_cast<int8_t>(s->q_dtype);
+  hdr.kv_dtype = static_cast<int8_t>(s->kv_dtype);
+  hdr.out_dtype = static_cast<int8_t>(s->out_dtype);
   std::memcpy(base, &hdr, sizeof(hdr));
   auto* items = reinterpret_cast<WorkItem*>(base + items_off);
   auto* groups = reinterpret_cast<MergeGroup*>(base + groups_off);
@@ -416,5 +457,14 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
       p = end;
     }
   }
+  return AUG_OK;
+}
+
+extern "C" aug_status aug_attn_workspace_size(const aug_attn_shape* s, const aug_batch_desc* b,
+                                              int32_t kv_split_tokens, size_t* bytes) {
+  if (!bytes) return fail(AUG_ERR_INVALID, "aug_attn_workspace_size: bytes is NULL");
+  aug_attn_plan_info info;
+  if (aug_status st = aug_attn_plan(s, b, kv_split_tokens, nullptr, 0, &info); st != AUG_OK) return st;
+  *bytes = static_cast<size_t>(info.workspace_bytes);
   return AUG_OK;
 }

@@ -7,12 +7,14 @@
 namespace aug {
 
 constexpr int32_t kPlanMagic = 0x4E4C5041;  // "APLN"
-constexpr int32_t kPlanVersion = 2;
+constexpr int32_t kPlanVersion = 3;
 constexpr int32_t kBlock = 16;              // tokens per KV block
 constexpr int32_t kKeyTile = 64;            // keys per MFMA tile (4 blocks)
 constexpr int32_t kTileRows = 128;          // query rows (positions x group heads) per MFMA tile
 constexpr int32_t kTileSpanMin = 256;       // a tile is never split into spans shorter than this
 constexpr int32_t kTileSpanMax = 8192;      // longest key span of one tile item (its block ids fit in LDS)
+constexpr int32_t kMaxContext = 1 << 24;    // longest context of one request the planner accepts
+constexpr int32_t kMaxSplit = 1 << 24;      // largest requested decode split (keys per work item)
 
 enum ItemKind : int32_t {
   kRowItem = 0,   // one query row (all heads of one KV head group) against a key span, VALU
@@ -33,7 +35,15 @@ struct PlanHeader {          // 64 bytes
   int32_t counters_offset;   // int32 per merge group, zero in the image
   int32_t append_offset;     // AppendItem list (16-byte aligned)
   int32_t num_append_items;
-  int32_t reserved[3];
+  // the layer shape the image was planned for
+  int16_t num_q_heads;
+  int16_t num_kv_heads;
+  int16_t head_dim;
+  int8_t q_dtype;
+  int8_t kv_dtype;
+  int8_t out_dtype;
+  int8_t reserved0;
+  int16_t reserved1;
 };
 
 struct WorkItem {            // 48 bytes

@@ -37,7 +37,7 @@ def ablation(make_former: Callable[[dict], Callable], make_lifecycle: Callable[[
     for order in orders:
         for dynamic in modes:
             t0 = time.perf_counter()
-            run = run_budget(budget, make_former(former_params(budget, dynamic, ORDERS[order])),
+            run = run_budget(budget, make_former(former_params(budget, dynamic, ORDERS[order], chunk_cap=512)),
                              make_lifecycle(), seed=seed, dynamic=dynamic, max_steps=max_steps, rate=rate,
                              max_preemptions=1_000_000, admit_whole_prompt=admit_whole_prompt)
             m = dict(run.metrics)

@@ -10,9 +10,11 @@ former -- any callable, normally the library's -- over it through
 many query tokens and how many keys. This module only chooses and lays out
 batches; the budget, costs, priorities and packing come from the former.
 
-Budgets below what the trace needs leave the loop overloaded: requests pile
-up until the pool thrashes. Such a run stops at ``max_steps`` iterations (or
-when the loop reports thrashing) and is marked incomplete.
+Every budget of the sweep serves the whole trace at 3 requests per second
+(prefill chunks are capped at half the budget). A budget too small for a
+heavier trace leaves the loop overloaded: requests pile up until the pool
+thrashes. Such a run stops at ``max_steps`` iterations (or when the loop
+reports thrashing) and is marked incomplete.
 """
 
 from __future__ import annotations
@@ -32,12 +34,24 @@ POOL_BLOCKS = 16384          # the serving loop's pool (blocks of 16 tokens)
 # Former parameters of the sweep (field names of the former's parameter
 # record); ``t_max`` is the budget being swept, and the dynamic mode clips the
 # memory-derived budget to [0.5, 2] x t_max while the static mode pins it.
-FORMER_PARAMS = dict(beta=5e-5, chunk_cap=512, t_iter=0.02, fwd_a=0.0175, fwd_b=20.5e-9,
-                     swap_s_per_tok=4.1e-8, n_fwd_max=1)
+FORMER_PARAMS = dict(beta=5e-5, t_iter=0.02, fwd_a=0.0175, fwd_b=20.5e-9, swap_s_per_tok=4.1e-8,
+                     n_fwd_max=1)
 
 
-def former_params(budget: int, dynamic: bool = True, order: int = 0) -> dict:
-    p = dict(FORMER_PARAMS, t_max=int(budget), order=int(order))
+def sweep_chunk_cap(budget: int) -> int:
+    """Prefill tokens one request may take per iteration under reference
+    budget T_max: half of it (at least 64). A prompt, a call's returned tokens
+    or a recomputed context then never fills a batch on its own, so decodes
+    always fit beside a chunk (with a fixed 512-token cap, budget 256 could
+    place a chunk only in an empty batch and could not serve the trace), and
+    larger budgets take longer chunks, as an engine without chunking would
+    take a whole prompt that fits its token limit."""
+    return max(64, int(budget) // 2)
+
+
+def former_params(budget: int, dynamic: bool = True, order: int = 0, chunk_cap: Optional[int] = None) -> dict:
+    p = dict(FORMER_PARAMS, t_max=int(budget), order=int(order),
+             chunk_cap=int(sweep_chunk_cap(budget) if chunk_cap is None else chunk_cap))
     p.update(beta_low=0.5, beta_high=2.0) if dynamic else p.update(beta_low=1.0, beta_high=1.0)
     return p
 

@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol():
     L = aug.lib()
     for name in declared:
         assert hasattr(L, name), name
-    assert aug.aug_abi_version() >> 16 == 1
+    assert aug.aug_abi_version() >> 16 == 2
     assert aug.aug_status_string(aug.AUG_ERR_NO_SPACE) == "AUG_ERR_NO_SPACE"
 
 
@@ -37,7 +37,7 @@ def _shape(b):
 
 def _decode_plan(plan):
     hdr = plan[:64].view(np.int32)
-    assert hdr[0] == 0x4E4C5041 and hdr[1] == 2
+    assert hdr[0] == 0x4E4C5041 and hdr[1] == 3
     n_items, n_groups = hdr[2], hdr[4]
     item_t = np.dtype([("kvh", "<i2"), ("kind", "i1"), ("res", "i1"), ("q_row0", "<i4"),
                        ("n_rows", "<i2"), ("stride", "<i2"), ("kb", "<i4"), ("ke", "<i4"),
@@ -181,6 +181,10 @@ def test_park_and_attention_reject_bad_arguments_without_touching_the_gpu():
     assert st == aug.AUG_ERR_INVALID             # fp8 without scales
     assert L.aug_kv_park(aug.C.byref(s), None, None, None, None, None, None, 0, 50, None, 0, None, 0,
                          None) == aug.AUG_OK     # nothing to do
+    # the host copy of the ids is required, so that every id is checked before a launch
+    for f in (L.aug_kv_park, L.aug_kv_resume):
+        st = f(aug.C.byref(s), 8, 8, None, None, 8, None, 3, 50, 8, 1 << 30, 8, 1 << 20, None)
+        assert st == aug.AUG_ERR_INVALID and "block_ids_host" in aug.aug_last_error()
     b = synth.make_tiny_mixed(seed=0)
     info, _ = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks)
     if info.num_partials == 0:
@@ -193,6 +197,87 @@ def test_park_and_attention_reject_bad_arguments_without_touching_the_gpu():
     st = L.aug_attn_mixed(aug.C.byref(_shape(b)), aug.C.byref(info), None, 8, 8, 8, None, None, 8,
                           b.num_pool_blocks, 8, 8, 1 << 30, None)
     assert st == aug.AUG_ERR_INVALID
+
+
+def test_plan_header_and_info_record_the_shape():
+    b = synth.make_mixed_8b(seed=1, n_dec=8, n_pre=1, n_pool_blocks=4096)
+    info, plan = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks)
+    hdr16 = plan[52:58].view(np.int16)
+    assert hdr16.tolist() == [32, 8, 128]
+    assert plan[58:61].view(np.int8).tolist() == [aug.AUG_BF16] * 3
+    assert (info.num_q_heads, info.num_kv_heads, info.head_dim) == (32, 8, 128)
+    assert (info.q_dtype, info.kv_dtype, info.out_dtype) == (aug.AUG_BF16,) * 3
+
+
+def test_workspace_size_query_matches_the_plan():
+    rng = np.random.default_rng(2)
+    ctx = [int(c) for c in rng.integers(1, 6000, 40)] + [700, 3000]
+    b = make_batch_from_lengths("ws", [1] * 40 + [100, 512], ctx, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                                q_dtype="bf16", kv_dtype="bf16", out_dtype="bf16",
+                                n_pool_blocks=sum(-(-c // 16) for c in ctx) + 8, seed=2)
+    for split in (0, 32, 256):
+        info, _ = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
+                                    b.block_ids, kv_split_tokens=split)
+        ws = aug.aug_attn_workspace_size(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
+                                         b.block_ids, kv_split_tokens=split)
+        assert ws == info.workspace_bytes
+        assert (ws > 0) == (info.num_partials > 0)
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_workspace_size(_shape(b), b.q_start, b.ctx_len[:-1] * 0, b.bt_start, b.num_pool_blocks)
+    assert e.value.status == aug.AUG_ERR_INVALID
+    L = aug.lib()
+    assert L.aug_attn_workspace_size(aug.C.byref(_shape(b)), None, 0, None) == aug.AUG_ERR_INVALID
+
+
+@pytest.mark.parametrize("split", [2 ** 31 - 1, 2 ** 31 - 100, 2 ** 24 + 1])
+def test_plan_rejects_a_huge_requested_split(split):
+    """A requested split near INT32_MAX must be refused, not overflow the
+    span arithmetic (which once divided by zero)."""
+    b = synth.make_tiny_mixed(seed=0)
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
+                          kv_split_tokens=split)
+    assert e.value.status == aug.AUG_ERR_INVALID and "kv_split_tokens" in str(e.value)
+    info, _ = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
+                                kv_split_tokens=2 ** 24)
+    assert info.kv_split_tokens == 2 ** 24
+
+
+def test_plan_rejects_contexts_beyond_its_limit():
+    s = aug.make_shape(8, 8, 64, "bf16", "bf16", "bf16", 0.125)
+    ctx = 2 ** 24 + 1
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_plan(s, [0, 1], [ctx], [0, -(-ctx // 16)], 1 << 21)
+    assert e.value.status == aug.AUG_ERR_UNSUPPORTED
+
+
+def test_a_plan_for_one_shape_is_refused_for_another():
+    """A plan built for 8 query heads per KV head (or any other head count,
+    head_dim or dtype set) is refused by a call with another shape, before
+    anything is launched: its items, partial sizes and workspace would not fit."""
+    L = aug.lib()
+    q_lens, ctx_lens = [40, 1, 1], [300, 700, 2100]
+    s4 = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)    # G = 4
+    b = make_batch_from_lengths("shape", q_lens, ctx_lens, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                                q_dtype="bf16", kv_dtype="bf16", out_dtype="bf16", n_pool_blocks=256, seed=4)
+    info, _ = aug.aug_attn_plan(s4, b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks, kv_split_tokens=64)
+    assert info.num_partials > 0
+    others = [aug.make_shape(64, 8, 128, "bf16", "bf16", "bf16", 0.088),     # G = 8
+              aug.make_shape(32, 4, 128, "bf16", "bf16", "bf16", 0.088),     # other KV heads
+              aug.make_shape(32, 8, 64, "bf16", "bf16", "bf16", 0.125),      # other head_dim
+              aug.make_shape(32, 8, 128, "bf16", "fp8", "bf16", 0.088)]      # other KV dtype
+    for s in others:
+        st = L.aug_attn_mixed(aug.C.byref(s), aug.C.byref(info), 8, 8, 8, 8, 8, 8, 8, b.num_pool_blocks, 8, 8,
+                              1 << 40, None)
+        assert st == aug.AUG_ERR_INVALID and "plan was built for" in aug.aug_last_error()
+        st = L.aug_kv_append(aug.C.byref(s), aug.C.byref(info), 8, 8, 8, 8, 8, 8, 8, 8, b.num_pool_blocks, None)
+        assert st == aug.AUG_ERR_INVALID and "plan was built for" in aug.aug_last_error()
+    # the softmax scale is not part of the plan: another scale is accepted by the checks
+    # (a NULL output pointer then stops the call, still before any launch)
+    s4b = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.5)
+    st = L.aug_attn_mixed(aug.C.byref(s4b), aug.C.byref(info), 8, 8, 8, 8, None, None, 8, b.num_pool_blocks,
+                          None, 8, 1 << 40, None)
+    assert st == aug.AUG_ERR_INVALID and "NULL" in aug.aug_last_error()
 
 
 def test_kv_append_rejects_bad_arguments_without_touching_the_gpu():

@@ -117,6 +117,47 @@ def test_lock_step_on_a_prefix_of_the_full_size_trace(budget):
     assert all(sum(s.q_len) <= s.budget for s in steps)
 
 
+def _lock_step_whole_trace(budget, dynamic):
+    """Serve the whole 2000-request sweep trace with both formers in lock
+    step; returns (finished requests, iterations, whether the loop stopped
+    because it was thrashing)."""
+    p = params_for(budget, dynamic)
+    loop = ServingLoop(make_trace(n=2000, seed=0, rate=3.0),
+                       SimConfig(num_blocks=sweep.POOL_BLOCKS, max_preemptions=200), LockstepLifecycle())
+    try:
+        loop.run(lockstep(oracle_former(p), library_former(p)))
+        thrashing = False
+    except RuntimeError as e:
+        if "thrashing" not in str(e):
+            raise
+        thrashing = True
+    return len(loop.done), len(loop.steps), thrashing
+
+
+@pytest.mark.slow
+def test_lock_step_over_the_whole_sweep_trace_at_every_budget():
+    """The oracle former and the library's agree (ids, token counts, theta
+    bit for bit, resume / park / free lists, policies, budgets) at every
+    iteration of the whole 2000-request trace of the budget sweep, for every
+    budget, in dynamic and static mode (about 25k iterations each). Every run
+    serves all 2000 requests except static mode at budget 256: a budget pinned
+    at 256 tokens cannot keep up with 3 requests per second, and both formers
+    agree at every iteration until the loop reports thrashing. The twelve
+    runs go to worker processes."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
+    jobs = [(b, d) for b in sweep.BUDGETS for d in (True, False)]
+    workers = max(1, min(len(jobs), len(os.sched_getaffinity(0))))
+    with cf.ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn")) as ex:
+        results = list(ex.map(_lock_step_whole_trace, *zip(*jobs)))
+    for (budget, dynamic), (finished, iters, thrashing) in zip(jobs, results):
+        if (budget, dynamic) == (256, False):
+            assert thrashing and iters > 5000, (finished, iters)
+        else:
+            assert finished == 2000 and not thrashing, (budget, dynamic, finished)
+            assert iters > 20000, (budget, dynamic, iters)
+
+
 def test_serving_former_marshals_like_the_test_driver():
     """The runtime's former callable (used by the benchmark and the GPU sweep)
     returns the same plans as the test driver's, which is checked against the
@@ -137,15 +178,26 @@ def test_serving_former_marshals_like_the_test_driver():
     assert len(loop.run(both, max_steps=300)) == 300
 
 
-def test_sweep_budgets_from_512_serve_the_whole_trace():
-    """Every request of the 2000-request trace finishes under budget 512 with
-    the 16,384-block pool; budget 256 overloads it (the loop stops early)."""
+def test_every_sweep_budget_serves_the_whole_trace_with_its_own_batches():
+    """Every request of the 2000-request trace finishes under every budget of
+    the sweep (16,384-block pool, chunks capped at half the budget), and each
+    budget forms batches of its own: the largest formed batch grows with the
+    budget, and budgets 4096 and 8192 form prefill-dominated batches that no
+    smaller budget can hold. A fixed 512-token chunk cap starves budget 256
+    (a chunk then fits only in an empty batch), which the loop reports."""
     from paper_2512_04013_amd import runtime as rt
-    run = sweep.run_budget(512, rt.serving_former(**sweep.former_params(512)), rt.serving_lifecycle())
-    assert run.complete and run.finished == 2000
-    assert all(sum(s.q_len) <= s.budget for s in run.steps)
-    small = sweep.run_budget(256, rt.serving_former(**sweep.former_params(256)), rt.serving_lifecycle(),
-                             max_steps=2000)
+    largest, biggest_prefill = [], []
+    for budget in sweep.BUDGETS:
+        run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), rt.serving_lifecycle())
+        assert run.complete and run.finished == 2000, budget
+        assert all(sum(s.q_len) <= s.budget for s in run.steps)
+        assert all(max(s.q_len) <= sweep.sweep_chunk_cap(budget) for s in run.steps)
+        largest.append(max(sum(s.q_len) for s in run.steps))
+        biggest_prefill.append(max(sum(q for q in s.q_len if q > 1) for s in run.steps))
+    assert all(a < b for a, b in zip(largest, largest[1:])), largest
+    assert biggest_prefill[-1] > biggest_prefill[-2] > 2048 >= biggest_prefill[2], biggest_prefill
+    small = sweep.run_budget(256, rt.serving_former(**sweep.former_params(256, chunk_cap=512)),
+                             rt.serving_lifecycle(), max_steps=2000)
     assert not small.complete
 
 
