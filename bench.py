@@ -10,9 +10,13 @@ their resume and park on their own, after the steps, and report them in
 ``park_resume`` as GB/s of the host link beside a plain pinned-memory copy of
 the same size; those host transfers are not part of ``value``.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode-8b]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload mixed-8b] [--also a,b]
 
-Prints one JSON line. ``value`` is query tokens per second of whole steps;
+Prints one JSON line. The main workload is the mixed batch of 3 x 512-row
+prefill chunks and 512 decodes under a 2048-token budget on the 8B-shaped
+layer; the decode-only batch, the long-context split-K batch and the
+prefill-dominated 64/8-head fp8 batch follow in the same run, each reported
+under ``workloads`` with its own roofline. ``value`` is query tokens per second of whole steps;
 ``roofline`` relates the attention launches' algorithmic bytes (each KV byte
 a request reads counted once, plus Q, O and block ids) to their duration,
 measured with HIP events on the launch stream; ``cpu_baseline`` times the
@@ -54,6 +58,8 @@ WORKLOADS = {
     # every budget 256 ... 8192: a sample of the formed batches replayed on one pool
     "budget-sweep-fp8": 6,
 }
+# timed after the main (mixed-batch) workload in the default run, each with its own roofline
+DEFAULT_ALSO = ("decode-8b", "long-context-8b", "prefill-fp8-64x8")
 
 
 def algorithmic_bytes(b) -> float:
@@ -357,8 +363,7 @@ def budget_sweep(args, log):
     for budget in sweep.BUDGETS:
         t0 = time.time()
         run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), rt.serving_lifecycle(),
-                               seed=args.seed,
-                               max_steps=4000 if budget == 256 else 40_000)
+                               seed=args.seed, max_steps=40_000)
         n = len(run.steps)
         pick = sorted(set(np.linspace(0, n - 1, min(n, args.sweep_batches)).astype(int).tolist())
                       | {sweep.select_steps(run.steps, 0, 0)[k] for k in ("most_tokens", "most_prefill")})
@@ -396,6 +401,7 @@ def budget_sweep(args, log):
     t_all, q_all, bytes_all, flops_all, wall_all = 0.0, 0, 0.0, 0.0, 0.0
     for budget, (run, pick) in runs.items():
         evs, qsum, nbytes, nflops = [], 0, 0.0, 0.0
+        kinds = []          # per replayed batch: (prefill-dominated?, bytes, flops)
         torch.cuda.synchronize()
         w0 = time.perf_counter()
         for k, i in enumerate(pick):
@@ -434,12 +440,24 @@ def budget_sweep(args, log):
             b.num_kv_heads, b.num_q_heads, b.head_dim = hkv, hq, d
             b.kv_dtype, b.q_dtype, b.out_dtype = "fp8", "bf16", "bf16"
             qsum += b.total_q
-            nbytes += algorithmic_bytes(b)
-            nflops += prefill_flops(b)
+            bb, ff = algorithmic_bytes(b), prefill_flops(b)
+            nbytes += bb
+            nflops += ff
+            kinds.append((ff / (MFMA_BF16_PEAK_TFS * 1e12) > bb / (HBM_PEAK_GBS * 1e9), bb, ff))
         torch.cuda.synchronize()
         wall = time.perf_counter() - w0
-        t = sum(a.elapsed_time(c) for a, c in evs) * 1e-3
+        times = [a.elapsed_time(c) * 1e-3 for a, c in evs]
+        t = sum(times)
+        by_kind = {}
+        for label, pre in (("prefill_dominated", True), ("decode_dominated", False)):
+            sel = [(tt, bb, ff) for tt, (p_dom, bb, ff) in zip(times, kinds) if p_dom == pre]
+            if sel:
+                ts = sum(x[0] for x in sel)
+                by_kind[label] = {"batches": len(sel), "attn_us_per_batch": round(1e6 * ts / len(sel), 1),
+                                  "mfma_frac": round(sum(x[2] for x in sel) / ts / (MFMA_BF16_PEAK_TFS * 1e12), 4),
+                                  "hbm_frac": round(sum(x[1] for x in sel) / ts / (HBM_PEAK_GBS * 1e9), 4)}
         results[budget] = {"batches_formed": len(run.steps), "trace_complete": bool(run.complete),
+                           "by_bound": by_kind,
                            "batches_replayed": len(pick), "query_tokens": int(qsum),
                            "attn_query_tokens_per_s": round(qsum / t, 1), "step_query_tokens_per_s": round(qsum / wall, 1),
                            "hbm_frac": round(nbytes / t / (HBM_PEAK_GBS * 1e9), 4),
@@ -478,52 +496,19 @@ def budget_sweep(args, log):
     print(json.dumps(result), flush=True)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="decode-8b", choices=sorted(WORKLOADS))
-    ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--kv-split", type=int, default=0, help="keys per decode work item (0: planner's choice)")
-    ap.add_argument("--pool-copies", type=int, default=0,
-                    help="copies of the KV pool used in turn (0: enough for 1 GiB of KV reads between "
-                         "two uses of one copy, at most 8)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-park-resume", action="store_true",
-                    help="skip the separate park/resume timing of workloads that move paused requests")
-    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
-    ap.add_argument("--sweep-batches", type=int, default=200,
-                    help="budget-sweep-fp8: formed batches replayed per budget")
-    ap.add_argument("--layers", type=int, default=8,
-                    help="after the steps, time this many layers of the planned batch (each an append and "
-                         "an attention call on its own pool copy) launched one by one and as one HIP graph "
-                         "(0: skip)")
-    ap.add_argument("--copy-probe-mib", type=int, default=0,
-                    help="before timing, copy a buffer of this many MiB a few times (a kernel of known "
-                         "traffic for calibrating hardware byte counters)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the step needs no "
-                                   "collectives and multi-GPU runs are not part of it",
-                          "n_gpus": args.gpus}))
-        sys.exit(2)
-
+def run_workload(name: str, args, log, full: bool = True) -> dict:
+    """Time ``args.steps`` whole steps of one workload (after ``args.warmup``
+    untimed ones) and return its result record: query tokens per second of
+    whole steps, the attention call's roofline and the KV append's rate; with
+    ``full`` also park/resume, the several-layer timing and the CPU oracle."""
     import torch
     import paper_2512_04013_amd as aug
     from paper_2512_04013_amd import runtime as rt
     import synth
 
-    def log(msg):
-        print(f"[bench] {msg}", file=sys.stderr, flush=True)
-
-    torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
-    if args.workload == "budget-sweep-fp8":
-        budget_sweep(args, log)
-        return
     t0 = time.time()
-    b, t_max = make_workload(args.workload, args.seed, log)
+    b, t_max = make_workload(name, args.seed, log)
     log(f"workload {b.name}: {b.num_reqs} requests, {b.total_q} query rows, "
         f"{int(b.ctx_len.sum())} context tokens ({time.time() - t0:.1f} s to generate)")
     shape, kv, q, bids = rt.upload_batch(b, device=dev)
@@ -551,7 +536,7 @@ def main():
     ev = []
     ev_append = []
     # the step's new K/V rows, written into the pool ahead of its attention
-    new_std = 1.0 / np.sqrt(b.head_dim) if WORKLOADS[args.workload] != 1 else 1.0
+    new_std = 1.0 / np.sqrt(b.head_dim) if WORKLOADS[name] != 1 else 1.0
     k_new_h, v_new_h = synth.make_new_kv(b, seed=args.seed + 7, std=new_std)
     new_dt = "f32" if b.kv_dtype == "f32" else "bf16"
     k_new = rt.to_device_array(k_new_h, new_dt, dev)
@@ -674,14 +659,80 @@ def main():
         "launch_ms_median": round(float(np.median(app_ms)), 4),
         "gbs": round(app_bytes / (float(app_ms.mean()) * 1e-3) / 1e9, 1),
         "frac_hbm": round(app_bytes / (float(app_ms.mean()) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-    if getattr(b, "park", None) is not None and len(b.park.resume_blocks) and not args.no_park_resume:
+    if full and getattr(b, "park", None) is not None and len(b.park.resume_blocks) and not args.no_park_resume:
         result["park_resume"] = park_resume_rates(b, kv, log)
-    if args.layers > 0:
+    if full and args.layers > 0:
         result["layers"] = time_layers(args.layers, shape, info, plan_dev, k_new, v_new, q, pools, bids,
                                        kv.num_pool_blocks, out, ws_dev, stream, log)
-    if not args.no_cpu_baseline:
+    if full and not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         result["cpu_baseline"] = cpu_baseline(b, args.cpu_budget_s)
+    gc.unfreeze()
+    return result
+
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mixed-8b", choices=sorted(WORKLOADS))
+    ap.add_argument("--also", default=None,
+                    help="comma-separated workloads timed after the main one in the same run, each reported "
+                         "with its own roofline under 'workloads' (default for mixed-8b: " +
+                         ",".join(DEFAULT_ALSO) + "; 'none' for no others)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--kv-split", type=int, default=0, help="keys per decode work item (0: planner's choice)")
+    ap.add_argument("--pool-copies", type=int, default=0,
+                    help="copies of the KV pool used in turn (0: enough for 1 GiB of KV reads between "
+                         "two uses of one copy, at most 8)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-park-resume", action="store_true",
+                    help="skip the separate park/resume timing of workloads that move paused requests")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--sweep-batches", type=int, default=200,
+                    help="budget-sweep-fp8: formed batches replayed per budget")
+    ap.add_argument("--layers", type=int, default=8,
+                    help="after the steps, time this many layers of the planned batch (each an append and "
+                         "an attention call on its own pool copy) launched one by one and as one HIP graph "
+                         "(0: skip)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="before timing, copy a buffer of this many MiB a few times (a kernel of known "
+                         "traffic for calibrating hardware byte counters)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the step needs no "
+                                   "collectives and multi-GPU runs are not part of it",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    torch.cuda.set_device(0)
+    if args.workload == "budget-sweep-fp8":
+        budget_sweep(args, log)
+        return
+    result = run_workload(args.workload, args, log, full=True)
+    if args.also is None:
+        also = list(DEFAULT_ALSO) if args.workload == "mixed-8b" else []
+    else:
+        also = [w for w in args.also.split(",") if w and w != "none"]
+    if also:
+        result["workloads"] = {}
+    for name in also:
+        if name not in WORKLOADS or name in ("budget-sweep-fp8", args.workload):
+            raise SystemExit(f"--also: {name} is not a single-batch workload other than the main one")
+        gc.collect()
+        torch.cuda.empty_cache()
+        sub = run_workload(name, args, log, full=False)
+        keep = ("value", "unit", "steps", "warmup", "ms_per_step", "dtype", "config", "roofline", "kv_append")
+        result["workloads"][sub["config"]["workload"]] = {k: sub[k] for k in keep}
+        log(f"{name}: {sub['value']:.0f} query-tokens/s, {sub['roofline']['unit']} frac "
+            f"{sub['roofline']['frac']}")
     print(json.dumps(result), flush=True)
 
 

@@ -139,13 +139,14 @@ def select_steps(steps: Sequence[StepRecord], n_random: int, seed: int) -> Dict[
 
 
 def batch_for_step(step: StepRecord, seed: int, name: str = "sweep-64x8-fp8",
-                   n_pool_blocks: Optional[int] = None) -> AttnBatch:
+                   n_pool_blocks: Optional[int] = None, sharp: bool = False) -> AttnBatch:
     """Lay one formed batch out on the 64/8-head fp8 layer: bf16 Q ~ N(0,1),
-    K/V ~ N(0,1)/sqrt(128) encoded per block (scale max|x|/448), blocks dealt
-    from a random permutation of the pool, unused slots NaN."""
+    K/V ~ N(0,1)/sqrt(128) (N(0,1) when ``sharp``) encoded per block (scale
+    max|x|/448), blocks dealt from a random permutation of the pool, unused
+    slots NaN."""
     need = int(sum(-(-c // 16) for c in step.ctx_len))
     pool = n_pool_blocks or max(POOL_BLOCKS, need + 64)
     return make_batch_from_lengths(
         name, step.q_len, step.ctx_len, num_q_heads=HEADS_Q, num_kv_heads=HEADS_KV,
         head_dim=HEAD_DIM, q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16", n_pool_blocks=pool,
-        seed=seed, kv_std=1.0 / np.sqrt(HEAD_DIM))
+        seed=seed, kv_std=1.0 if sharp else 1.0 / np.sqrt(HEAD_DIM))

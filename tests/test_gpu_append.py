@@ -11,7 +11,7 @@ import synth  # noqa: E402
 from oracle import attention as oa  # noqa: E402
 from oracle import kvappend  # noqa: E402
 from synth.attn_inputs import make_batch_from_lengths  # noqa: E402
-from tests.gpu_util import compare, rows_of, say  # noqa: E402
+from tests.gpu_util import compare, say  # noqa: E402
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -83,10 +83,13 @@ def test_append_is_bit_exact_and_attention_reads_it(case):
     if std <= 1.0:
         compare(got, want, qd, what=f"attention after append, case {case}")
         return
-    # New rows far larger than the configured N(0,1) inputs: the MFMA tile
-    # path rounds each probability to bf16 (relative 2^-9), which moves an
-    # output by at most 2^-9 * max|v - o| / (1 - 2^-9) <= 2^-8 * max|v|, plus
-    # half an ulp of the bf16 output. The fixed gates assume |v| of a few units.
+    # New rows far larger than the configured N(0,1) inputs. A departure from
+    # the stated gate, on purpose: the MFMA paths round each probability to
+    # bf16 (relative 2^-9) before the P.V product, which moves an output by at
+    # most 2^-9 * max|v - o| / (1 - 2^-9) <= 2^-8 * max|v|, plus half an ulp
+    # of the bf16 output; the fixed 1e-2 gate therefore holds only while
+    # max|v| stays within a few units (it does for every configured workload,
+    # sharp inputs included), and this case is held to that derived bound.
     vmax = max(np.abs(oa.materialise_kv(v, vs, kv, b.blocks_of(r), int(b.ctx_len[r]))).max()
                for r in range(b.num_reqs))
     bound = 2.0 ** -8 * vmax + 2.0 ** -9 * np.abs(want) + 1e-6
@@ -175,11 +178,9 @@ def test_append_full_size(which):
     others = np.setdiff1d(np.random.default_rng(1).choice(b.num_pool_blocks, 4000, replace=False), touched)
     ot = torch.from_numpy(others).cuda()
     _same(_bytes(kvp.k_cache[ot]), np.ascontiguousarray(b.k_cache[others]).view(np.uint8).reshape(-1), "kvp.k_cache[ot]")
-    # attention of sampled requests over the appended cache
+    # attention of every row over the appended cache
     b.k_cache[touched], b.v_cache[touched] = k, v
     if b.kv_dtype == "fp8":
         b.k_scale[touched], b.v_scale[touched] = ks, vs
-    reqs = [0, 1] + sorted(int(r) for r in np.random.default_rng(2).choice(
-        np.arange(3 if which == "mixed-8b-bf16" else 14, b.num_reqs), 24, replace=False))
-    want = oa.attention_for(b, requests=reqs)
-    compare(rt.to_host_f64(out), want, "bf16", rows=rows_of(b, reqs), what=f"{which} after append")
+    want = oa.attention_for(b)
+    compare(rt.to_host_f64(out), want, "bf16", what=f"{which} after append (all {b.total_q} rows)")
