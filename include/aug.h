@@ -219,6 +219,33 @@ aug_status aug_attn_mixed(const aug_attn_shape* shape, const aug_attn_plan_info*
                           const int32_t* block_ids, int32_t num_pool_blocks, void* out,
                           void* workspace, size_t workspace_bytes, void* stream);
 
+/* Bytes of the library's own device array for split-K partials, used by
+ * aug_attn_mixed_noalloc (64 MiB per GPU the library runs on). */
+#define AUG_NOALLOC_SCRATCH_BYTES (64ull << 20)
+
+/* aug_attn_mixed for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same launch, arguments and results, but the split-K partials live in a
+ * file-scope device array of the library (AUG_NOALLOC_SCRATCH_BYTES per GPU,
+ * held until the process ends) instead of a caller workspace. The caller
+ * still passes the plan image, inputs and output. The array's device address
+ * is looked up once per device, on the first call made with that device
+ * current; `stream` must belong to the current device. Nothing in the array
+ * needs to start at zero (every partial is written before it is read), and
+ * it keeps the last call's contents. All calls on one GPU share the array:
+ * calls that overlap in time on that GPU (other streams, other threads)
+ * race and must be serialised by the caller. Allocates nothing (no
+ * hipMalloc, no hipFree, no allocating library call).
+ * Errors: those of aug_attn_mixed; AUG_ERR_NO_SPACE when the plan's
+ * info->workspace_bytes exceeds AUG_NOALLOC_SCRATCH_BYTES (plan with a larger
+ * kv_split_tokens, or use aug_attn_mixed); AUG_ERR_HIP when the array's
+ * address cannot be obtained or the launch fails. */
+aug_status aug_attn_mixed_noalloc(const aug_attn_shape* shape, const aug_attn_plan_info* info,
+                                  void* plan_dev, const void* q, const void* k_cache,
+                                  const void* v_cache, const float* k_scale, const float* v_scale,
+                                  const int32_t* block_ids, int32_t num_pool_blocks, void* out,
+                                  void* stream);
+
 /* Append the step's new K/V rows to the paged cache, before the attention of
  * the same step reads them: every query row is a token the forward pass
  * produced (the chunk or decode token scheduled in Algorithm 1, step (5)).

@@ -35,7 +35,7 @@ AUG_POL_NONE, AUG_PRESERVE, AUG_DISCARD, AUG_SWAP = 0, 1, 2, 3
 DTYPE_CODES = {"f32": AUG_F32, "bf16": AUG_BF16, "fp8": AUG_FP8_E4M3FN}
 
 EXPORTED = ["aug_request_arrive", "aug_request_return", "aug_attn_plan", "aug_attn_workspace_size",
-            "aug_plan_upload", "aug_attn_mixed",
+            "aug_plan_upload", "aug_attn_mixed", "aug_attn_mixed_noalloc",
             "aug_kv_append", "aug_kv_record_bytes", "aug_kv_park", "aug_kv_resume", "aug_form_batch",
             "aug_status_string", "aug_last_error", "aug_abi_version"]
 
@@ -129,6 +129,8 @@ def lib():
                                           C.POINTER(C.c_size_t)]
     L.aug_attn_mixed.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P,
                                  P, P, P, C.c_int32, P, P, C.c_size_t, P]
+    L.aug_attn_mixed_noalloc.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P,
+                                         P, P, P, C.c_int32, P, P]
     L.aug_kv_append.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P, P,
                                 P, P, P, C.c_int32, P]
     L.aug_plan_upload.argtypes = [P, P, C.c_size_t, P]
@@ -142,7 +144,8 @@ def lib():
                                  C.POINTER(aug_batch_plan)]
     L.aug_request_arrive.argtypes = [P, C.c_int64, C.c_double, C.c_int32, C.c_int32, C.c_double, C.c_int32]
     L.aug_request_return.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_double, C.c_int32]
-    for f in ("aug_attn_plan", "aug_attn_workspace_size", "aug_plan_upload", "aug_attn_mixed", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
+    for f in ("aug_attn_plan", "aug_attn_workspace_size", "aug_plan_upload", "aug_attn_mixed",
+              "aug_attn_mixed_noalloc", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
               "aug_form_batch", "aug_request_arrive", "aug_request_return"):
         getattr(L, f).restype = C.c_int
     L.aug_status_string.argtypes = [C.c_int]
@@ -297,6 +300,19 @@ def aug_attn_mixed(shape: aug_attn_shape, info: aug_attn_plan_info, plan_dev, q,
                                 _ptr(k_cache), _ptr(v_cache), _ptr(k_scale), _ptr(v_scale),
                                 _ptr(block_ids), int(num_pool_blocks), _ptr(out), _ptr(workspace),
                                 int(workspace_bytes), st), "aug_attn_mixed")
+
+
+def aug_attn_mixed_noalloc(shape: aug_attn_shape, info: aug_attn_plan_info, plan_dev, q, k_cache, v_cache,
+                           k_scale, v_scale, block_ids, num_pool_blocks: int, out, stream=None):
+    """Enqueue the attention of a planned batch with the split-K partials in
+    the library's own device array (no workspace argument)."""
+    st = _stream(stream, q, out)
+    _check(lib().aug_attn_mixed_noalloc(C.byref(shape), C.byref(info), _ptr(plan_dev), _ptr(q), _ptr(k_cache),
+                                        _ptr(v_cache), _ptr(k_scale), _ptr(v_scale), _ptr(block_ids),
+                                        int(num_pool_blocks), _ptr(out), st), "aug_attn_mixed_noalloc")
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 def aug_kv_append(shape: aug_attn_shape, info: aug_attn_plan_info, plan_dev, k_new, v_new, k_cache,

@@ -42,6 +42,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <type_traits>
 
 #include "aug.h"
@@ -1328,14 +1329,10 @@ aug_status dispatch_dg(int d, int g, const AttnArgs& a, const aug_attn_plan_info
   return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: head_dim %d with group %d", d, g);
 }
 
-}  // namespace
-
-extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_plan_info* info,
-                                     void* plan_dev, const void* q, const void* k_cache,
-                                     const void* v_cache, const float* k_scale, const float* v_scale,
-                                     const int32_t* block_ids, int32_t num_pool_blocks, void* out,
-                                     void* workspace, size_t workspace_bytes, void* stream) {
-  const char* who = "aug_attn_mixed";
+// Checks shared by both entry points (everything but the workspace).
+aug_status check_call(const char* who, const aug_attn_shape* s, const aug_attn_plan_info* info, void* plan_dev,
+                      const void* q, const void* k_cache, const void* v_cache, const float* k_scale,
+                      const float* v_scale, const int32_t* block_ids, int32_t num_pool_blocks, void* out) {
   if (aug_status st = aug::check_shape(s, who); st != AUG_OK) return st;
   if (aug_status st = aug::check_plan_info(info, s, who); st != AUG_OK) return st;
   if (info->num_items == 0) return AUG_OK;
@@ -1344,10 +1341,13 @@ extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_pla
   if (s->kv_dtype == AUG_FP8_E4M3FN && (!k_scale || !v_scale))
     return aug::fail(AUG_ERR_INVALID, "%s: fp8 KV needs k_scale and v_scale", who);
   if (num_pool_blocks < 1) return aug::fail(AUG_ERR_INVALID, "%s: empty pool", who);
-  if (info->num_partials > 0 && (!workspace || workspace_bytes < static_cast<size_t>(info->workspace_bytes)))
-    return aug::fail(AUG_ERR_NO_SPACE, "%s: workspace %zu < %lld bytes", who, workspace_bytes,
-                     (long long)info->workspace_bytes);
+  return AUG_OK;
+}
 
+aug_status enqueue(const aug_attn_shape* s, const aug_attn_plan_info* info, void* plan_dev, const void* q,
+                   const void* k_cache, const void* v_cache, const float* k_scale, const float* v_scale,
+                   const int32_t* block_ids, int32_t num_pool_blocks, void* out, void* workspace,
+                   void* stream) {
   AttnArgs a{};
   auto* base = static_cast<unsigned char*>(plan_dev);
   const size_t groups_off = sizeof(aug::PlanHeader) + static_cast<size_t>(info->num_items) * sizeof(WorkItem);
@@ -1372,4 +1372,81 @@ extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_pla
   if (s->kv_dtype == AUG_F32) return dispatch_dg<KV_F32, AUG_F32, AUG_F32>(s->head_dim, g, a, *info, st);
   if (s->kv_dtype == AUG_BF16) return dispatch_dg<KV_BF16, AUG_BF16, AUG_BF16>(s->head_dim, g, a, *info, st);
   return dispatch_dg<KV_FP8, AUG_BF16, AUG_BF16>(s->head_dim, g, a, *info, st);
+}
+
+}  // namespace
+
+extern "C" aug_status aug_attn_mixed(const aug_attn_shape* s, const aug_attn_plan_info* info,
+                                     void* plan_dev, const void* q, const void* k_cache,
+                                     const void* v_cache, const float* k_scale, const float* v_scale,
+                                     const int32_t* block_ids, int32_t num_pool_blocks, void* out,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  const char* who = "aug_attn_mixed";
+  if (aug_status st = check_call(who, s, info, plan_dev, q, k_cache, v_cache, k_scale, v_scale, block_ids,
+                                 num_pool_blocks, out);
+      st != AUG_OK || info->num_items == 0)
+    return st;
+  if (info->num_partials > 0 && (!workspace || workspace_bytes < static_cast<size_t>(info->workspace_bytes)))
+    return aug::fail(AUG_ERR_NO_SPACE, "%s: workspace %zu < %lld bytes", who, workspace_bytes,
+                     (long long)info->workspace_bytes);
+  return enqueue(s, info, plan_dev, q, k_cache, v_cache, k_scale, v_scale, block_ids, num_pool_blocks, out,
+                 workspace, stream);
+}
+
+// ---------------------------------------------------------------------------
+// the same launch with the split-K partials in a library-owned device array
+// ---------------------------------------------------------------------------
+
+// Device memory for the split-K partials of aug_attn_mixed_noalloc: one copy
+// per GPU, held until the process ends. In host code this name stands for the
+// array only symbolically; its device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[AUG_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device, looked up on the
+// first call there and kept.
+aug_status scratch_on_current_device(void** ptr, const char* who) {
+  int dev = -1;
+  if (hipError_t e = hipGetDevice(&dev); e != hipSuccess)
+    return aug::fail(AUG_ERR_HIP, "%s: hipGetDevice: %s", who, hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return aug::fail(AUG_ERR_UNSUPPORTED, "%s: device %d", who, dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)); e != hipSuccess || !p)
+      return aug::fail(AUG_ERR_HIP, "%s: hipGetSymbolAddress of the scratch array: %s", who,
+                       hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return AUG_OK;
+}
+
+}  // namespace
+
+extern "C" aug_status aug_attn_mixed_noalloc(const aug_attn_shape* s, const aug_attn_plan_info* info,
+                                             void* plan_dev, const void* q, const void* k_cache,
+                                             const void* v_cache, const float* k_scale, const float* v_scale,
+                                             const int32_t* block_ids, int32_t num_pool_blocks, void* out,
+                                             void* stream) {
+  const char* who = "aug_attn_mixed_noalloc";
+  if (aug_status st = check_call(who, s, info, plan_dev, q, k_cache, v_cache, k_scale, v_scale, block_ids,
+                                 num_pool_blocks, out);
+      st != AUG_OK || info->num_items == 0)
+    return st;
+  if (info->workspace_bytes > static_cast<int64_t>(AUG_NOALLOC_SCRATCH_BYTES))
+    return aug::fail(AUG_ERR_NO_SPACE, "%s: the plan needs %lld bytes of split-K partials, more than the %lld "
+                     "of the library's scratch array (plan with a larger kv_split_tokens, or call "
+                     "aug_attn_mixed with a workspace)", who, (long long)info->workspace_bytes,
+                     (long long)AUG_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if (info->num_partials > 0)
+    if (aug_status st = scratch_on_current_device(&ws, who); st != AUG_OK) return st;
+  return enqueue(s, info, plan_dev, q, k_cache, v_cache, k_scale, v_scale, block_ids, num_pool_blocks, out, ws,
+                 stream);
 }

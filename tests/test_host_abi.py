@@ -280,6 +280,23 @@ def test_a_plan_for_one_shape_is_refused_for_another():
     assert st == aug.AUG_ERR_INVALID and "NULL" in aug.aug_last_error()
 
 
+def test_noalloc_attention_rejects_bad_arguments_without_touching_the_gpu():
+    L = aug.lib()
+    b = synth.make_tiny_mixed(seed=0)
+    info, _ = aug.aug_attn_plan(_shape(b), b.q_start, b.ctx_len, b.bt_start, b.num_pool_blocks,
+                                kv_split_tokens=32)
+    assert info.num_partials > 0
+    args = (8, 8, 8, 8, None, None, 8, b.num_pool_blocks, 8, None)
+    big = aug.aug_attn_plan_info.from_buffer_copy(info)
+    big.workspace_bytes = aug.NOALLOC_SCRATCH_BYTES + 256
+    assert L.aug_attn_mixed_noalloc(aug.C.byref(_shape(b)), aug.C.byref(big), *args) == aug.AUG_ERR_NO_SPACE
+    assert "scratch" in aug.aug_last_error()
+    assert L.aug_attn_mixed_noalloc(aug.C.byref(_shape(b)), aug.C.byref(info), None, *args[1:]) == \
+        aug.AUG_ERR_INVALID
+    other = aug.make_shape(8, 4, 64, "f32", "f32", "f32", 0.125)
+    assert L.aug_attn_mixed_noalloc(aug.C.byref(other), aug.C.byref(info), *args) == aug.AUG_ERR_INVALID
+
+
 def test_kv_append_rejects_bad_arguments_without_touching_the_gpu():
     L = aug.lib()
     b = synth.make_tiny_mixed(seed=0)
