@@ -525,7 +525,13 @@ def run_workload(name: str, args, log, full: bool = True) -> dict:
     recs = request_records(b, aug)
     used_blocks = int(np.sum((b.ctx_len.astype(np.int64) + 15) // 16))
     free_blocks = b.num_pool_blocks - used_blocks
-    params = aug.former_params(t_max=t_max, beta_low=0.5, beta_high=1.0, chunk_cap=512)
+    if WORKLOADS[name] == 5:
+        # a trace-formed batch is re-formed with the sweep's own former parameters
+        # (dynamic budget up to twice T_max, chunks capped at half of it)
+        from synth import sweep
+        params = aug.former_params(**sweep.former_params(t_max))
+    else:
+        params = aug.former_params(t_max=t_max, beta_low=0.5, beta_high=1.0, chunk_cap=512)
     stream = torch.cuda.current_stream(dev)
     plan_dev = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
     plan_host = [torch.empty(64 << 20, dtype=torch.uint8, pin_memory=True) for _ in range(2)]
