@@ -143,8 +143,22 @@ typedef struct {
   int32_t q_dtype;
   int32_t kv_dtype;
   int32_t out_dtype;
-  int32_t reserved;
+  int32_t row_path;          /* aug_row_path the plan's row items run on (VALU or MFMA, resolved) */
 } aug_attn_plan_info;
+
+/* Where the row items (decode rows) of a plan run. Groups of eight query
+ * heads per KV head with head_dim 128 and bf16 or fp8 KV can run their
+ * products on 16x16 bf16 MFMAs (the vector ALUs cannot keep up with eight
+ * heads of fp8 KV); every other shape runs on the vector ALUs. AUTO takes
+ * MFMA where it can, VALU otherwise. */
+typedef enum { AUG_ROWS_AUTO = 0, AUG_ROWS_VALU = 1, AUG_ROWS_MFMA = 2 } aug_row_path;
+
+/* Planner options (aug_attn_plan_opts). */
+typedef struct {
+  int32_t kv_split_tokens;   /* as the argument of aug_attn_plan */
+  int32_t row_path;          /* aug_row_path */
+  int32_t reserved[2];       /* zero */
+} aug_plan_options;
 
 /* Validate a formed batch and write its work list ("plan image") to
  * plan_host, which needs info->plan_bytes bytes (call once with
@@ -164,6 +178,15 @@ typedef struct {
 aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batch,
                          int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
                          aug_attn_plan_info* info);
+
+/* aug_attn_plan with options: opts->kv_split_tokens as above, and the path
+ * the row items run on (info->row_path records the resolved choice, which
+ * aug_attn_mixed follows). Same image layout and errors, plus
+ * AUG_ERR_UNSUPPORTED for AUG_ROWS_MFMA on a shape without that path and
+ * AUG_ERR_INVALID for an unknown row path or non-zero reserved fields. */
+aug_status aug_attn_plan_opts(const aug_attn_shape* shape, const aug_batch_desc* batch,
+                              const aug_plan_options* opts, void* plan_host, size_t plan_cap,
+                              aug_attn_plan_info* info);
 
 /* Device workspace (split-K partials, in bytes) that aug_attn_mixed needs for
  * this batch with this split: the planner's size query, the same validation

@@ -31,10 +31,12 @@ AUG_OK, AUG_ERR_INVALID, AUG_ERR_UNSUPPORTED, AUG_ERR_NO_SPACE, AUG_ERR_HIP = 0,
 AUG_F32, AUG_BF16, AUG_FP8_E4M3FN = 0, 1, 2
 AUG_WAITING, AUG_RUNNING, AUG_SWAPPED, AUG_PAUSED = 0, 1, 2, 3
 AUG_POL_NONE, AUG_PRESERVE, AUG_DISCARD, AUG_SWAP = 0, 1, 2, 3
+AUG_ROWS_AUTO, AUG_ROWS_VALU, AUG_ROWS_MFMA = 0, 1, 2
 
 DTYPE_CODES = {"f32": AUG_F32, "bf16": AUG_BF16, "fp8": AUG_FP8_E4M3FN}
 
-EXPORTED = ["aug_request_arrive", "aug_request_return", "aug_attn_plan", "aug_attn_workspace_size",
+EXPORTED = ["aug_request_arrive", "aug_request_return", "aug_attn_plan", "aug_attn_plan_opts",
+            "aug_attn_workspace_size",
             "aug_plan_upload", "aug_attn_mixed", "aug_attn_mixed_noalloc",
             "aug_kv_append", "aug_kv_record_bytes", "aug_kv_park", "aug_kv_resume", "aug_form_batch",
             "aug_status_string", "aug_last_error", "aug_abi_version"]
@@ -68,7 +70,11 @@ class aug_attn_plan_info(C.Structure):
                 ("num_tile_merge_groups", C.c_int32), ("num_append_items", C.c_int32),
                 ("num_q_heads", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
                 ("q_dtype", C.c_int32), ("kv_dtype", C.c_int32), ("out_dtype", C.c_int32),
-                ("reserved", C.c_int32)]
+                ("row_path", C.c_int32)]
+
+
+class aug_plan_options(C.Structure):
+    _fields_ = [("kv_split_tokens", C.c_int32), ("row_path", C.c_int32), ("reserved", C.c_int32 * 2)]
 
 
 class aug_request(C.Structure):
@@ -125,6 +131,8 @@ def lib():
     P = C.c_void_p
     L.aug_attn_plan.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_batch_desc), C.c_int32, P,
                                 C.c_size_t, C.POINTER(aug_attn_plan_info)]
+    L.aug_attn_plan_opts.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_batch_desc),
+                                     C.POINTER(aug_plan_options), P, C.c_size_t, C.POINTER(aug_attn_plan_info)]
     L.aug_attn_workspace_size.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_batch_desc), C.c_int32,
                                           C.POINTER(C.c_size_t)]
     L.aug_attn_mixed.argtypes = [C.POINTER(aug_attn_shape), C.POINTER(aug_attn_plan_info), P, P, P, P,
@@ -144,7 +152,7 @@ def lib():
                                  C.POINTER(aug_batch_plan)]
     L.aug_request_arrive.argtypes = [P, C.c_int64, C.c_double, C.c_int32, C.c_int32, C.c_double, C.c_int32]
     L.aug_request_return.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_double, C.c_int32]
-    for f in ("aug_attn_plan", "aug_attn_workspace_size", "aug_plan_upload", "aug_attn_mixed",
+    for f in ("aug_attn_plan", "aug_attn_plan_opts", "aug_attn_workspace_size", "aug_plan_upload", "aug_attn_mixed",
               "aug_attn_mixed_noalloc", "aug_kv_append", "aug_kv_park", "aug_kv_resume",
               "aug_form_batch", "aug_request_arrive", "aug_request_return"):
         getattr(L, f).restype = C.c_int
@@ -244,19 +252,25 @@ def _batch_desc(q_start, ctx_len, bt_start, num_pool_blocks, block_ids=None):
 
 
 def aug_attn_plan(shape: aug_attn_shape, q_start, ctx_len, bt_start, num_pool_blocks: int,
-                  block_ids=None, kv_split_tokens: int = 0):
-    """Validate a batch (host arrays) and build its plan image.
-    Returns (info, plan) with plan a numpy uint8 array of info.plan_bytes bytes."""
+                  block_ids=None, kv_split_tokens: int = 0, row_path: int = AUG_ROWS_AUTO):
+    """Validate a batch (host arrays) and build its plan image (aug_attn_plan,
+    or aug_attn_plan_opts when a row path is requested). Returns (info, plan)
+    with plan a numpy uint8 array of info.plan_bytes bytes."""
     L = lib()
     desc, keep = _batch_desc(q_start, ctx_len, bt_start, num_pool_blocks, block_ids)
+    opts = aug_plan_options(int(kv_split_tokens), int(row_path))
     info = aug_attn_plan_info()
     # one scratch image per thread: ctypes releases the GIL during the call
     buf = getattr(_plan_scratch, "buf", None)
     if buf is None:
         buf = _plan_scratch.buf = np.zeros(1 << 20, dtype=np.uint8)
     while True:
-        st = L.aug_attn_plan(C.byref(shape), C.byref(desc), int(kv_split_tokens), buf.ctypes.data,
-                             buf.nbytes, C.byref(info))
+        if row_path == AUG_ROWS_AUTO:
+            st = L.aug_attn_plan(C.byref(shape), C.byref(desc), int(kv_split_tokens), buf.ctypes.data,
+                                 buf.nbytes, C.byref(info))
+        else:
+            st = L.aug_attn_plan_opts(C.byref(shape), C.byref(desc), C.byref(opts), buf.ctypes.data, buf.nbytes,
+                                      C.byref(info))
         if st == AUG_ERR_NO_SPACE and info.plan_bytes > buf.nbytes:
             buf = _plan_scratch.buf = np.zeros(int(info.plan_bytes) * 2, dtype=np.uint8)
             continue

@@ -68,10 +68,6 @@ constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running max
 // denominator always share one reference, so the result is unchanged.
 constexpr float kRescaleSlack = 8.0f;
 constexpr int kThreads = 256;
-#ifndef AUG_ROW_MFMA
-#define AUG_ROW_MFMA 1
-#endif
-constexpr bool kRowMfma = AUG_ROW_MFMA;   // 8-way GQA decode rows on MFMA
 
 
 enum : int { KV_F32 = 0, KV_BF16 = 1, KV_FP8 = 2 };
@@ -1249,7 +1245,14 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
 template <int D, int G>
 constexpr int row_lds_bytes() { return (kThreads / 64) * G * (D + 2) * 4; }
 
-template <int KVT, int D, int G, int QT, int OT, bool TILES>
+// Whether row items of this instantiation can run on the 16x16 MFMA row
+// path (eight query heads per KV head, head_dim 128, bf16 or fp8 KV).
+template <int KVT, int D, int G, int QT>
+constexpr bool row_mfma_capable() {
+  return G == 8 && D == 128 && (KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16;
+}
+
+template <int KVT, int D, int G, int QT, int OT, bool TILES, bool ROW_MFMA>
 __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   constexpr int RB = row_lds_bytes<D, G>();
   constexpr int TB = TILES ? TileLds<D>::BYTES : 0;
@@ -1265,24 +1268,24 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   }
   // row items always fetch a wave's next block while the current one is
   // computed: short spans (small batches) are latency bound otherwise
-  if constexpr (kRowMfma && G == 8 && D == 128 && (KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16)
+  if constexpr (ROW_MFMA && row_mfma_capable<KVT, D, G, QT>())
     row_item_mfma<KVT, OT>(it, a, reinterpret_cast<float*>(smem));
   else
     row_item<KVT, D, G, QT, OT, true>(it, a, reinterpret_cast<float*>(smem));
 }
 
 // Batches without prefill tiles: row items only, sized for high occupancy.
-template <int KVT, int D, int G, int QT, int OT>
+template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
 __global__ __launch_bounds__(kThreads) void attn_rows_kernel(AttnArgs a) {
-  attn_body<KVT, D, G, QT, OT, false>(a);
+  attn_body<KVT, D, G, QT, OT, false, ROW_MFMA>(a);
 }
 
 // Mixed batches: MFMA tiles and row items in one launch. The tile path's
 // accumulators set the register budget (two waves per SIMD); the row path
 // spends the same budget on prefetching the next block.
-template <int KVT, int D, int G, int QT, int OT>
+template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mixed_kernel(AttnArgs a) {
-  attn_body<KVT, D, G, QT, OT, true>(a);
+  attn_body<KVT, D, G, QT, OT, true, ROW_MFMA>(a);
 }
 
 // Merge launch for split prefill tiles: one workgroup per (row, KV head)
@@ -1293,18 +1296,33 @@ __global__ __launch_bounds__(kThreads) void tile_merge_kernel(AttnArgs a) {
   merge_group<D, G, OT, kThreads>(a.groups[blockIdx.x], a.partials, a.out, a.hq, lds);
 }
 
+template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
+aug_status launch_rows(const AttnArgs& a, const aug_attn_plan_info& info, hipStream_t st) {
+  if (info.num_prefill_items > 0) {
+    if constexpr ((KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16) {
+      hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA>), dim3(info.num_items), dim3(kThreads), 0,
+                         st, a);
+    } else {
+      return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: plan has tiles for a dtype set without them");
+    }
+  } else {
+    hipLaunchKernelGGL((attn_rows_kernel<KVT, D, G, QT, OT, ROW_MFMA>), dim3(info.num_items), dim3(kThreads), 0, st,
+                       a);
+  }
+  return AUG_OK;
+}
+
 template <int KVT, int D, int G, int QT, int OT>
 aug_status launch(const AttnArgs& a, const aug_attn_plan_info& info, hipStream_t st) {
   if (info.num_items > 0) {
-    if (info.num_prefill_items > 0) {
-      if constexpr ((KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16) {
-        hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT>), dim3(info.num_items), dim3(kThreads), 0, st, a);
-      } else {
-        return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: plan has tiles for a dtype set without them");
-      }
+    aug_status rs;
+    if constexpr (row_mfma_capable<KVT, D, G, QT>()) {
+      rs = info.row_path == AUG_ROWS_VALU ? launch_rows<KVT, D, G, QT, OT, false>(a, info, st)
+                                          : launch_rows<KVT, D, G, QT, OT, true>(a, info, st);
     } else {
-      hipLaunchKernelGGL((attn_rows_kernel<KVT, D, G, QT, OT>), dim3(info.num_items), dim3(kThreads), 0, st, a);
+      rs = launch_rows<KVT, D, G, QT, OT, false>(a, info, st);
     }
+    if (rs != AUG_OK) return rs;
     if (hipError_t e = hipGetLastError(); e != hipSuccess)
       return aug::fail(AUG_ERR_HIP, "aug_attn_mixed: launch failed: %s", hipGetErrorString(e));
   }

@@ -32,6 +32,11 @@ bool dtype_set_supported(const aug_attn_shape& s) {
   return false;
 }
 
+bool row_mfma_supported(const aug_attn_shape& s) {
+  return s.num_q_heads == 8 * s.num_kv_heads && s.head_dim == 128 && s.q_dtype == AUG_BF16 &&
+         (s.kv_dtype == AUG_BF16 || s.kv_dtype == AUG_FP8_E4M3FN);
+}
+
 bool tiles_supported(const aug_attn_shape& s) {
   return s.q_dtype == AUG_BF16 && (s.kv_dtype == AUG_BF16 || s.kv_dtype == AUG_FP8_E4M3FN);
 }
@@ -77,6 +82,8 @@ aug_status check_plan_info(const aug_attn_plan_info* info, const aug_attn_shape*
                 who, info->num_q_heads, info->num_kv_heads, info->head_dim, info->q_dtype, info->kv_dtype,
                 info->out_dtype, s->num_q_heads, s->num_kv_heads, s->head_dim, s->q_dtype, s->kv_dtype,
                 s->out_dtype);
+  if (info->row_path != AUG_ROWS_VALU && !(info->row_path == AUG_ROWS_MFMA && row_mfma_supported(*s)))
+    return fail(AUG_ERR_INVALID, "%s: info names row path %d, which this shape cannot run", who, info->row_path);
   return AUG_OK;
 }
 
@@ -130,8 +137,26 @@ using namespace aug;
 extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_desc* b,
                                     int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
                                     aug_attn_plan_info* info) {
+  const aug_plan_options opts{kv_split_tokens, AUG_ROWS_AUTO, {0, 0}};
+  return aug_attn_plan_opts(s, b, &opts, plan_host, plan_cap, info);
+}
+
+extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batch_desc* b,
+                                         const aug_plan_options* opts, void* plan_host, size_t plan_cap,
+                                         aug_attn_plan_info* info) {
   const char* who = "aug_attn_plan";
   if (aug_status st = check_shape(s, who); st != AUG_OK) return st;
+  if (!opts) return fail(AUG_ERR_INVALID, "%s: options are NULL", who);
+  if (opts->reserved[0] != 0 || opts->reserved[1] != 0)
+    return fail(AUG_ERR_INVALID, "%s: reserved option fields must be zero", who);
+  const int32_t kv_split_tokens = opts->kv_split_tokens;
+  int32_t row_path = opts->row_path;
+  if (row_path != AUG_ROWS_AUTO && row_path != AUG_ROWS_VALU && row_path != AUG_ROWS_MFMA)
+    return fail(AUG_ERR_INVALID, "%s: unknown row path %d", who, row_path);
+  if (row_path == AUG_ROWS_MFMA && !row_mfma_supported(*s))
+    return fail(AUG_ERR_UNSUPPORTED, "%s: the MFMA row path needs 8 query heads per KV head, head_dim 128 and "
+                "bf16 or fp8 KV", who);
+  if (row_path == AUG_ROWS_AUTO) row_path = row_mfma_supported(*s) ? AUG_ROWS_MFMA : AUG_ROWS_VALU;
   if (!b || !info) return fail(AUG_ERR_INVALID, "%s: batch or info is NULL", who);
   const int32_t n = b->num_reqs;
   if (n < 0) return fail(AUG_ERR_INVALID, "%s: num_reqs %d < 0", who, n);
@@ -372,6 +397,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   info->q_dtype = s->q_dtype;
   info->kv_dtype = s->kv_dtype;
   info->out_dtype = s->out_dtype;
+  info->row_path = row_path;
   if (!plan_host) return AUG_OK;
   if (plan_cap < static_cast<size_t>(plan_bytes))
     return fail(AUG_ERR_NO_SPACE, "%s: plan buffer %zu < %lld bytes", who, plan_cap,
@@ -398,6 +424,7 @@ extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_des
   hdr.q_dtype = static_cast<int8_t>(s->q_dtype);
   hdr.kv_dtype = static_cast<int8_t>(s->kv_dtype);
   hdr.out_dtype = static_cast<int8_t>(s->out_dtype);
+  hdr.row_path = static_cast<int8_t>(row_path);
   std::memcpy(base, &hdr, sizeof(hdr));
   auto* items = reinterpret_cast<WorkItem*>(base + items_off);
   auto* groups = reinterpret_cast<MergeGroup*>(base + groups_off);

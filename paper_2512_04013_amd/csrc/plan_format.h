@@ -42,7 +42,7 @@ struct PlanHeader {          // 64 bytes
   int8_t q_dtype;
   int8_t kv_dtype;
   int8_t out_dtype;
-  int8_t reserved0;
+  int8_t row_path;           // aug_row_path of the row items (resolved)
   int16_t reserved1;
 };
 

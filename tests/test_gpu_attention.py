@@ -17,11 +17,11 @@ pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
 
 
-def _run(batch, kv_split=0, staging_bytes=1 << 26):
+def _run(batch, kv_split=0, staging_bytes=1 << 26, row_path=0):
     from paper_2512_04013_amd import runtime as rt
     shape, kv, q, bids = rt.upload_batch(batch, staging_bytes=staging_bytes)
     att = rt.MixedAttention(shape, kv, batch.q_start, batch.ctx_len, batch.bt_start, batch.block_ids,
-                            bids, kv_split_tokens=kv_split)
+                            bids, kv_split_tokens=kv_split, row_path=row_path)
     out = att.run(q)
     torch.cuda.synchronize()
     return rt.to_host_f64(out), att
@@ -117,10 +117,12 @@ def test_decode_8b_full(decode_8b, split):
 
 @pytest.mark.parametrize("kv", ["fp8", "bf16"])
 @pytest.mark.parametrize("sharp", [False, True])
-def test_gqa8_decode_batch_full_size(kv, sharp):
+@pytest.mark.parametrize("row_path", [2, 1])
+def test_gqa8_decode_batch_full_size(kv, sharp, row_path):
     """512 decodes on the 64/8-head layer (the shape of the budget sweep),
     contexts lognormal (median 2500, sigma 0.8, cap 16384): the 8-way grouped
-    decode rows run on the MFMA row path. Every row against the oracle."""
+    decode rows on the MFMA row path (the planner's default for this shape)
+    and on the vector-ALU row path. Every row against the oracle."""
     if kv == "fp8":
         b = synth.make_decode_gqa8_fp8(seed=0, sharp=sharp)      # the decode-fp8-64x8 bench workload
         ctx = b.ctx_len.astype(int)
@@ -131,9 +133,10 @@ def test_gqa8_decode_batch_full_size(kv, sharp):
                                     head_dim=128, q_dtype="bf16", kv_dtype=kv, out_dtype="bf16",
                                     n_pool_blocks=int(sum(-(-c // 16) for c in ctx)) + 64, seed=22,
                                     kv_std=1.0 if sharp else 1.0 / np.sqrt(128.0))
-    say(f"[gqa8 decode] kv={kv} sharp={sharp} keys={int(ctx.sum())}")
-    got, att = _run(b)
-    compare(got, oa.attention_for(b), "bf16", what=f"gqa8 decode {kv} sharp={sharp} (all 512 rows)")
+    say(f"[gqa8 decode] kv={kv} sharp={sharp} row_path={row_path} keys={int(ctx.sum())}")
+    got, att = _run(b, row_path=row_path)
+    assert att.info.row_path == row_path
+    compare(got, oa.attention_for(b), "bf16", what=f"gqa8 decode {kv} sharp={sharp} row path {row_path} (all 512 rows)")
 
 
 def test_decode_8b_sharp_full():

@@ -280,6 +280,41 @@ def test_a_plan_for_one_shape_is_refused_for_another():
     assert st == aug.AUG_ERR_INVALID and "NULL" in aug.aug_last_error()
 
 
+def test_row_path_option_resolves_and_is_checked():
+    """AUTO runs eight-head groups (head_dim 128, bf16 or fp8 KV) on the MFMA
+    row path and everything else on the vector ALUs; VALU can be asked for
+    anywhere, MFMA only where it exists. The resolved path is in the info and
+    the plan header, and a call refuses an info naming a path its shape lacks."""
+    L = aug.lib()
+    ctx = [700, 3000, 17]
+    q_start, bt_start = [0, 1, 2, 3], np.concatenate([[0], np.cumsum([-(-c // 16) for c in ctx])])
+    pool = int(bt_start[-1]) + 4
+    g8 = aug.make_shape(64, 8, 128, "bf16", "fp8", "bf16", 0.088)
+    g4 = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)
+    info, plan = aug.aug_attn_plan(g8, q_start, ctx, bt_start, pool)
+    assert info.row_path == aug.AUG_ROWS_MFMA and plan[61] == aug.AUG_ROWS_MFMA
+    info, plan = aug.aug_attn_plan(g8, q_start, ctx, bt_start, pool, row_path=aug.AUG_ROWS_VALU)
+    assert info.row_path == aug.AUG_ROWS_VALU and plan[61] == aug.AUG_ROWS_VALU
+    info4, _ = aug.aug_attn_plan(g4, q_start, ctx, bt_start, pool)
+    assert info4.row_path == aug.AUG_ROWS_VALU
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_plan(g4, q_start, ctx, bt_start, pool, row_path=aug.AUG_ROWS_MFMA)
+    assert e.value.status == aug.AUG_ERR_UNSUPPORTED
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_plan(g8, q_start, ctx, bt_start, pool, row_path=7)
+    assert e.value.status == aug.AUG_ERR_INVALID
+    desc, keep = aug._batch_desc(q_start, ctx, bt_start, pool)
+    opts = aug.aug_plan_options(0, 0)
+    opts.reserved[1] = 3
+    out = aug.aug_attn_plan_info()
+    assert L.aug_attn_plan_opts(aug.C.byref(g8), aug.C.byref(desc), aug.C.byref(opts), None, 0,
+                                aug.C.byref(out)) == aug.AUG_ERR_INVALID
+    bad = aug.aug_attn_plan_info.from_buffer_copy(info4)
+    bad.row_path = aug.AUG_ROWS_MFMA
+    st = L.aug_attn_mixed(aug.C.byref(g4), aug.C.byref(bad), 8, 8, 8, 8, None, None, 8, pool, 8, 8, 1 << 40, None)
+    assert st == aug.AUG_ERR_INVALID and "row path" in aug.aug_last_error()
+
+
 def test_noalloc_attention_rejects_bad_arguments_without_touching_the_gpu():
     L = aug.lib()
     b = synth.make_tiny_mixed(seed=0)
