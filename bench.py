@@ -49,6 +49,9 @@ WORKLOADS = {
     # under an 8192-token budget, on the 64/8-head fp8-KV layer
     "sweep-prefill-fp8": 5,   # the batch with the most prefill query-key pairs
     "sweep-context-fp8": 5,   # the batch with the most context tokens
+    # a typical small batch: under a 512-token budget, the formed batch with the
+    # median number of context tokens
+    "sweep-median-512-fp8": 5,
     # 512 decodes on the same 64/8-head fp8 layer (decode-dominated, full size)
     "decode-fp8-64x8": 7,
     # prefill-dominated batches: 16 x 512-row chunks on the 64/8-head fp8
@@ -336,11 +339,15 @@ def make_workload(name: str, seed: int, log):
         return synth.make_config(cfg, seed=seed), 2048
     from synth import sweep
     from paper_2512_04013_amd import runtime as rt
-    budget = 8192
+    budget = 512 if name == "sweep-median-512-fp8" else 8192
     t0 = time.time()
     run = sweep.run_budget(budget, rt.serving_former(**sweep.former_params(budget)), rt.serving_lifecycle(),
                            seed=seed)
-    pick = sweep.select_steps(run.steps, 0, seed)["most_prefill" if name == "sweep-prefill-fp8" else "most_context"]
+    if name == "sweep-median-512-fp8":
+        ctx = np.array([sum(st.ctx_len) for st in run.steps])
+        pick = int(np.argsort(ctx, kind="stable")[len(ctx) // 2])
+    else:
+        pick = sweep.select_steps(run.steps, 0, seed)["most_prefill" if name == "sweep-prefill-fp8" else "most_context"]
     log(f"trace served under budget {budget}: {len(run.steps)} batches in {time.time() - t0:.1f} s; "
         f"batch {pick} chosen")
     return sweep.batch_for_step(run.steps[pick], seed=seed + 1000, name=f"{name}-budget{budget}"), budget
