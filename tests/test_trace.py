@@ -117,12 +117,12 @@ def test_lock_step_on_a_prefix_of_the_full_size_trace(budget):
     assert all(sum(s.q_len) <= s.budget for s in steps)
 
 
-def _lock_step_whole_trace(budget, dynamic):
+def _lock_step_whole_trace(budget, dynamic, seed=0):
     """Serve the whole 2000-request sweep trace with both formers in lock
     step; returns (finished requests, iterations, whether the loop stopped
     because it was thrashing)."""
     p = params_for(budget, dynamic)
-    loop = ServingLoop(make_trace(n=2000, seed=0, rate=3.0),
+    loop = ServingLoop(make_trace(n=2000, seed=seed, rate=3.0),
                        SimConfig(num_blocks=sweep.POOL_BLOCKS, max_preemptions=200), LockstepLifecycle())
     try:
         loop.run(lockstep(oracle_former(p), library_former(p)))
@@ -139,23 +139,25 @@ def test_lock_step_over_the_whole_sweep_trace_at_every_budget():
     """The oracle former and the library's agree (ids, token counts, theta
     bit for bit, resume / park / free lists, policies, budgets) at every
     iteration of the whole 2000-request trace of the budget sweep, for every
-    budget, in dynamic and static mode (about 25k iterations each). Every run
-    serves all 2000 requests except static mode at budget 256: a budget pinned
-    at 256 tokens cannot keep up with 3 requests per second, and both formers
-    agree at every iteration until the loop reports thrashing. The twelve
-    runs go to worker processes."""
+    budget, in dynamic mode for trace seeds 0, 1 and 2 and in static mode for
+    seed 0 (23k-25k iterations each). Every run serves all 2000 requests
+    except static mode at budget 256: a budget pinned at 256 tokens cannot
+    keep up with 3 requests per second, and both formers agree at every
+    iteration until the loop reports thrashing. The 24 runs go to worker
+    processes."""
     import concurrent.futures as cf
     import multiprocessing as mp
-    jobs = [(b, d) for b in sweep.BUDGETS for d in (True, False)]
+    jobs = [(b, True, seed) for seed in (0, 1, 2) for b in sweep.BUDGETS] + [(b, False, 0) for b in sweep.BUDGETS]
+    jobs.sort(key=lambda j: (j[0] != 256, j[1]))     # the longest runs first
     workers = max(1, min(len(jobs), len(os.sched_getaffinity(0))))
     with cf.ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn")) as ex:
         results = list(ex.map(_lock_step_whole_trace, *zip(*jobs)))
-    for (budget, dynamic), (finished, iters, thrashing) in zip(jobs, results):
+    for (budget, dynamic, seed), (finished, iters, thrashing) in zip(jobs, results):
         if (budget, dynamic) == (256, False):
             assert thrashing and iters > 5000, (finished, iters)
         else:
-            assert finished == 2000 and not thrashing, (budget, dynamic, finished)
-            assert iters > 20000, (budget, dynamic, iters)
+            assert finished == 2000 and not thrashing, (budget, dynamic, seed, finished)
+            assert iters > 20000, (budget, dynamic, seed, iters)
 
 
 def test_serving_former_marshals_like_the_test_driver():
