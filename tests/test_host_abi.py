@@ -249,6 +249,31 @@ def test_plan_rejects_contexts_beyond_its_limit():
     with pytest.raises(AugError) as e:
         aug.aug_attn_plan(s, [0, 1], [ctx], [0, -(-ctx // 16)], 1 << 21)
     assert e.value.status == aug.AUG_ERR_UNSUPPORTED
+    # the limit itself is accepted: a decode and a 300-row chunk over 2^24 keys,
+    # every key of every row covered by the spans (largest requested split too)
+    ctx = 2 ** 24
+    for q_len, split in ((1, 0), (300, 0), (1, 2 ** 24)):
+        info, plan = aug.aug_attn_plan(s, [0, q_len], [ctx], [0, ctx // 16], 1 << 21, kv_split_tokens=split)
+        hdr, items, groups = _decode_plan(plan)
+        for j in (0, q_len - 1):
+            pos = ctx - q_len + j
+            mine = items[(items["kvh"] == 0) & (items["q_row0"] <= j) & (j < items["q_row0"] + items["n_rows"])]
+            spans = sorted((int(a), min(int(b), pos + 1)) for a, b in zip(mine["kb"], mine["ke"]) if a <= pos)
+            assert spans[0][0] == 0 and spans[-1][1] == pos + 1
+            assert all(x[1] == y[0] for x, y in zip(spans, spans[1:]))
+
+
+def test_empty_batches_launch_nothing():
+    L = aug.lib()
+    s = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)
+    info, plan = aug.aug_attn_plan(s, [0], [], [0], 64)
+    assert info.num_items == 0 and info.num_append_items == 0 and info.workspace_bytes == 0
+    assert aug.aug_attn_workspace_size(s, [0], [], [0], 64) == 0
+    # every device pointer NULL: nothing is launched, so nothing is dereferenced
+    assert L.aug_attn_mixed(aug.C.byref(s), aug.C.byref(info), None, None, None, None, None, None, None, 64, None,
+                            None, 0, None) == aug.AUG_OK
+    assert L.aug_attn_mixed_noalloc(aug.C.byref(s), aug.C.byref(info), None, None, None, None, None, None, None, 64,
+                                    None, None) == aug.AUG_OK
 
 
 def test_a_plan_for_one_shape_is_refused_for_another():
