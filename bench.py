@@ -636,14 +636,16 @@ def run_workload(name: str, args, log, full: bool = True, row_path: int = 0) -> 
     flops = prefill_flops(b)
     achieved_gbs = nbytes / (attn_ms * 1e-3) / 1e9
     achieved_tfs = flops / (attn_ms * 1e-3) / 1e12
+    # counters were taken with the planner's default row path only
+    traffic = measured_traffic(b.name) if row_path == 0 else None
     # the batch is bound by whichever roof its algorithmic work reaches first
     if flops / (MFMA_BF16_PEAK_TFS * 1e12) > nbytes / (HBM_PEAK_GBS * 1e9):
         roof = {"bound": "mfma", "achieved": round(achieved_tfs, 1), "peak": MFMA_BF16_PEAK_TFS,
                 "unit": "TFLOP/s", "frac": round(achieved_tfs / MFMA_BF16_PEAK_TFS, 4),
-                "traffic": measured_traffic(b.name), "hbm_gbs": round(achieved_gbs, 1)}
+                "traffic": traffic, "hbm_gbs": round(achieved_gbs, 1)}
     else:
         roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(b.name)}
+                "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic}
         if flops > 0:
             roof["prefill_mfma_tflops"] = round(achieved_tfs, 2)
     # decode rows' flops (4 D H_q per key): on the vector ALUs for up to four
