@@ -365,13 +365,12 @@ __device__ __forceinline__ void finish_split(const AttnArgs& a, int group, int n
 // o[G][D], running maximum and row sum to lds[wave][head][D + 2]; the waves'
 // results are merged (log-sum-exp) and stored as the output rows, or as the
 // item's split-K partial.
-template <int D, int G, int OT>
+template <int D, int G, int OT, int NW>
 __device__ __forceinline__ void row_merge_waves(const WorkItem& it, const AttnArgs& a, float* lds) {
   constexpr int ROW = D + 2;
   const int kvh = it.kvh;
   __syncthreads();
-  constexpr int NW = kThreads / 64;
-  for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
+  for (int idx = threadIdx.x; idx < G * D; idx += 64 * NW) {
     const int h = idx / D;
     const int d = idx % D;
     float mw[NW];
@@ -400,11 +399,11 @@ __device__ __forceinline__ void row_merge_waves(const WorkItem& it, const AttnAr
       }
     }
   }
-  if (it.part >= 0) finish_split<D, G, OT, kThreads>(a, it.group, 1, lds);
+  if (it.part >= 0) finish_split<D, G, OT, 64 * NW>(a, it.group, 1, lds);
 }
 
 
-template <int KVT, int D, int G, int QT, int OT, bool PREFETCH>
+template <int KVT, int D, int G, int QT, int OT, bool PREFETCH, int NW>
 __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   using F = KvFmt<KVT>;
   using M = RowMath<KVT, QT>;
@@ -450,7 +449,7 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
   // the K/V loads of a block never wait on the block-table load. With
   // PREFETCH the K/V of the next block are in flight too while the current
   // one is computed.
-  constexpr int kWaves = kThreads / 64;
+  constexpr int kWaves = NW;
   const int32_t* table = a.block_ids + it.bt_off + blk0;
   auto load_block = [&](int bid, elem_t* kr, elem_t* vr) {
     const bool ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
@@ -595,7 +594,7 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
       }
     }
   }
-  row_merge_waves<D, G, OT>(it, a, lds);
+  row_merge_waves<D, G, OT, NW>(it, a, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -709,7 +708,7 @@ template <> struct MfmaRowKv<KV_FP8> {
   }
 };
 
-template <int KVT, int OT>
+template <int KVT, int OT, int NW>
 __device__ void row_item_mfma(const WorkItem& it, const AttnArgs& a, float* lds) {
   constexpr int D = 128, G = 8;
   constexpr bool FP8 = KVT == KV_FP8;
@@ -745,7 +744,7 @@ __device__ void row_item_mfma(const WorkItem& it, const AttnArgs& a, float* lds)
   const char* vc = static_cast<const char*>(a.v_cache);
   const int64_t k_lane = (j * D + 32 * g) * EB;                          // token j, dims 32g..
   const int64_t v_lane = (4 * g * D + 8 * j) * EB;                       // tokens 4g.., dims 8j..
-  constexpr int kWaves = kThreads / 64;
+  constexpr int kWaves = NW;
   const int32_t* table = a.block_ids + it.bt_off + blk0;
   // a block's K and V, and (fp8) its two scales, loaded together so the
   // scales arrive with the data instead of a memory round trip later
@@ -853,7 +852,7 @@ __device__ void row_item_mfma(const WorkItem& it, const AttnArgs& a, float* lds)
       dst[D + 1] = l_tot;
     }
   }
-  row_merge_waves<D, G, OT>(it, a, lds);
+  row_merge_waves<D, G, OT, NW>(it, a, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -1242,8 +1241,8 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
 // kernels
 // ---------------------------------------------------------------------------
 
-template <int D, int G>
-constexpr int row_lds_bytes() { return (kThreads / 64) * G * (D + 2) * 4; }
+template <int D, int G, int NW>
+constexpr int row_lds_bytes() { return NW * G * (D + 2) * 4; }
 
 // Whether row items of this instantiation can run on the 16x16 MFMA row
 // path (eight query heads per KV head, head_dim 128, bf16 or fp8 KV).
@@ -1252,9 +1251,10 @@ constexpr bool row_mfma_capable() {
   return G == 8 && D == 128 && (KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16;
 }
 
-template <int KVT, int D, int G, int QT, int OT, bool TILES, bool ROW_MFMA>
+template <int KVT, int D, int G, int QT, int OT, bool TILES, bool ROW_MFMA, int NW>
 __device__ __forceinline__ void attn_body(const AttnArgs& a) {
-  constexpr int RB = row_lds_bytes<D, G>();
+  static_assert(!TILES || NW == kThreads / 64, "tile items run on four-wave workgroups");
+  constexpr int RB = row_lds_bytes<D, G, NW>();
   constexpr int TB = TILES ? TileLds<D>::BYTES : 0;
   static_assert(RB >= (merge_lds_floats(G) + 1) * 4 && (!TILES || TB >= (merge_lds_floats(G) + 1) * 4),
                 "a split item's workgroup merges in its own LDS");
@@ -1269,15 +1269,15 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   // row items always fetch a wave's next block while the current one is
   // computed: short spans (small batches) are latency bound otherwise
   if constexpr (ROW_MFMA && row_mfma_capable<KVT, D, G, QT>())
-    row_item_mfma<KVT, OT>(it, a, reinterpret_cast<float*>(smem));
+    row_item_mfma<KVT, OT, NW>(it, a, reinterpret_cast<float*>(smem));
   else
-    row_item<KVT, D, G, QT, OT, true>(it, a, reinterpret_cast<float*>(smem));
+    row_item<KVT, D, G, QT, OT, true, NW>(it, a, reinterpret_cast<float*>(smem));
 }
 
-// Batches without prefill tiles: row items only, sized for high occupancy.
-template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
-__global__ __launch_bounds__(kThreads) void attn_rows_kernel(AttnArgs a) {
-  attn_body<KVT, D, G, QT, OT, false, ROW_MFMA>(a);
+// Batches without prefill tiles: row items only, on workgroups of NW waves.
+template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_rows_kernel(AttnArgs a) {
+  attn_body<KVT, D, G, QT, OT, false, ROW_MFMA, NW>(a);
 }
 
 // Mixed batches: MFMA tiles and row items in one launch. The tile path's
@@ -1285,7 +1285,7 @@ __global__ __launch_bounds__(kThreads) void attn_rows_kernel(AttnArgs a) {
 // spends the same budget on prefetching the next block.
 template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mixed_kernel(AttnArgs a) {
-  attn_body<KVT, D, G, QT, OT, true, ROW_MFMA>(a);
+  attn_body<KVT, D, G, QT, OT, true, ROW_MFMA, kThreads / 64>(a);
 }
 
 // Merge launch for split prefill tiles: one workgroup per (row, KV head)
@@ -1306,8 +1306,14 @@ aug_status launch_rows(const AttnArgs& a, const aug_attn_plan_info& info, hipStr
       return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: plan has tiles for a dtype set without them");
     }
   } else {
-    hipLaunchKernelGGL((attn_rows_kernel<KVT, D, G, QT, OT, ROW_MFMA>), dim3(info.num_items), dim3(kThreads), 0, st,
-                       a);
+    // MFMA row items without tiles beside them run eight waves per
+    // workgroup (the planner gives them spans twice as long): a typical
+    // context is then one item merged in LDS instead of two or more spans
+    // merged through partials. The VALU row path keeps four waves: its
+    // register use would leave a compute unit a single eight-wave workgroup.
+    constexpr int NW = ROW_MFMA && row_mfma_capable<KVT, D, G, QT>() ? 8 : 4;
+    hipLaunchKernelGGL((attn_rows_kernel<KVT, D, G, QT, OT, ROW_MFMA, NW>), dim3(info.num_items), dim3(64 * NW), 0,
+                       st, a);
   }
   return AUG_OK;
 }

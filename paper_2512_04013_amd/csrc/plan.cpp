@@ -116,16 +116,19 @@ double merge_ns(int64_t partial_bytes) {
 // its total work spread evenly.
 double makespan_bound(double longest, double total) { return std::max(longest, total / kSlots); }
 
-int32_t choose_split(int64_t total_row_keys, int32_t requested) {
+int32_t choose_split(int64_t total_row_keys, int32_t requested, bool wide_rows) {
   if (requested > 0) return ((requested + kBlock - 1) / kBlock) * kBlock;   // requested <= kMaxSplit
   // About four row items per compute unit (256 CUs), but never spans under
   // 512 keys (on small batches an item's fixed latency, query load, state
   // merge and partial write, outweighs shorter streams); on large batches
   // spans of 4096 keys, long enough that those fixed costs are a few percent
   // of an item's streaming time while lognormal context mixes still balance.
-  int64_t s = (total_row_keys + 1023) / 1024;
-  s = std::max<int64_t>(s, 512);
-  s = std::min<int64_t>(s, 4096);
+  // Eight-wave row items (MFMA rows without tiles) take spans twice as long,
+  // so that each wave streams as many keys as in a four-wave item.
+  const int32_t f = wide_rows ? 2 : 1;
+  int64_t s = (total_row_keys + 1024 / f - 1) / (1024 / f);
+  s = std::max<int64_t>(s, 512 * f);
+  s = std::min<int64_t>(s, 4096 * f);
   return static_cast<int32_t>(((s + kBlock - 1) / kBlock) * kBlock);
 }
 
@@ -169,6 +172,7 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
   const int32_t hkv = s->num_kv_heads;
   const int32_t g = s->num_q_heads / hkv;
   int64_t total_row_keys = 0;
+  bool any_tiled = false;
   for (int32_t r = 0; r < n; ++r) {
     const int64_t q = static_cast<int64_t>(b->q_start[r + 1]) - b->q_start[r];
     const int64_t ctx = b->ctx_len[r];
@@ -193,6 +197,7 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
       }
     }
     const bool tiled = q > 1 && tiles_supported(*s);
+    any_tiled = any_tiled || tiled;
     if (!tiled) {
       // rows at positions ctx-q .. ctx-1 read pos+1 keys each
       total_row_keys += (q * (2 * ctx - q + 1) / 2) * hkv;
@@ -224,7 +229,8 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
       return fail(AUG_ERR_INVALID, "%s: block %d receives new tokens more than once", who, *dup);
   }
 
-  const int32_t split = choose_split(total_row_keys, kv_split_tokens);
+  // a launch without tiles runs MFMA row items on eight-wave workgroups
+  const int32_t split = choose_split(total_row_keys, kv_split_tokens, !any_tiled && row_path == AUG_ROWS_MFMA);
   const int32_t pos_per_tile = kTileRows / g;
   const int32_t kv_bytes_all = s->kv_dtype == AUG_F32 ? 4 : s->kv_dtype == AUG_BF16 ? 2 : 1;
 

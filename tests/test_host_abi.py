@@ -340,6 +340,29 @@ def test_row_path_option_resolves_and_is_checked():
     assert st == aug.AUG_ERR_INVALID and "row path" in aug.aug_last_error()
 
 
+def test_default_split_doubles_for_mfma_rows_without_tiles():
+    """A launch of MFMA row items alone runs eight-wave workgroups and takes
+    decode spans twice as long as four-wave row items: 1024 instead of 512
+    keys on a small batch, 8192 instead of 4096 on a large one. Row items
+    beside prefill tiles, and VALU row items, keep the four-wave spans; an
+    explicit split is taken as given."""
+    def plan(shape, q_len, ctx, **kw):
+        q_start = np.concatenate([[0], np.cumsum(q_len)])
+        bt_start = np.concatenate([[0], np.cumsum([-(-c // 16) for c in ctx])])
+        info, _ = aug.aug_attn_plan(shape, q_start, ctx, bt_start, int(bt_start[-1]) + 4, **kw)
+        return info
+    g8 = aug.make_shape(64, 8, 128, "bf16", "fp8", "bf16", 0.088)
+    small, large = [2000] * 20, [3000] * 512
+    assert plan(g8, [1] * 20, small).kv_split_tokens == 1024
+    assert plan(g8, [1] * 20, small, row_path=aug.AUG_ROWS_VALU).kv_split_tokens == 512
+    assert plan(g8, [1] * 19 + [64], small).kv_split_tokens == 512      # one prefill chunk: tiles
+    assert plan(g8, [1] * 512, large).kv_split_tokens == 8192
+    assert plan(g8, [1] * 512, large, row_path=aug.AUG_ROWS_VALU).kv_split_tokens == 4096
+    assert plan(g8, [1] * 20, small, kv_split_tokens=300).kv_split_tokens == 304
+    g4 = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)
+    assert plan(g4, [1] * 20, small).kv_split_tokens == 512
+
+
 def test_noalloc_attention_rejects_bad_arguments_without_touching_the_gpu():
     L = aug.lib()
     b = synth.make_tiny_mixed(seed=0)
