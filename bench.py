@@ -39,6 +39,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFS = 2516.6
+MFMA_FP8_PEAK_TFS = 2 * MFMA_BF16_PEAK_TFS
 
 WORKLOADS = {
     "tiny-mixed": 1,
@@ -63,8 +64,11 @@ WORKLOADS = {
 }
 # timed after the main (mixed-batch) workload in the default run, each with its own roofline
 # (a workload name followed by "@valu" runs its row items on the vector ALUs instead of the
-# planner's default, which is MFMA for eight query heads per KV head)
-DEFAULT_ALSO = ("decode-8b", "long-context-8b", "prefill-fp8-64x8", "decode-fp8-64x8", "decode-fp8-64x8@valu")
+# planner's default, which is MFMA for eight query heads per KV head; "@fp8qk" runs the
+# prefill tiles' score products on fp8 MFMAs, an opt-in arithmetic)
+DEFAULT_ALSO = ("decode-8b", "long-context-8b", "prefill-fp8-64x8", "prefill-fp8-64x8@fp8qk", "decode-fp8-64x8",
+                "decode-fp8-64x8@valu")
+PATHS = {"": (0, 0), "valu": (1, 0), "fp8qk": (0, 2)}   # suffix -> (row path, tile path)
 
 
 def algorithmic_bytes(b) -> float:
@@ -509,7 +513,7 @@ def budget_sweep(args, log):
     print(json.dumps(result), flush=True)
 
 
-def run_workload(name: str, args, log, full: bool = True, row_path: int = 0) -> dict:
+def run_workload(name: str, args, log, full: bool = True, row_path: int = 0, tile_path: int = 0) -> dict:
     """Time ``args.steps`` whole steps of one workload (after ``args.warmup``
     untimed ones) and return its result record: query tokens per second of
     whole steps, the attention call's roofline and the KV append's rate; with
@@ -573,7 +577,8 @@ def run_workload(name: str, args, log, full: bool = True, row_path: int = 0) -> 
         q_start = np.zeros(len(sel) + 1, np.int32)
         q_start[1:] = np.cumsum(q_len[sel])
         info, plan = aug.aug_attn_plan(shape, q_start, b.ctx_len, b.bt_start, kv.num_pool_blocks,
-                                       None, kv_split_tokens=args.kv_split, row_path=row_path)
+                                       None, kv_split_tokens=args.kv_split, row_path=row_path,
+                                       tile_path=tile_path)
         # double-buffered pinned staging: a buffer is rewritten only after the
         # copy that last read it has completed
         slot = i & 1
@@ -636,13 +641,20 @@ def run_workload(name: str, args, log, full: bool = True, row_path: int = 0) -> 
     flops = prefill_flops(b)
     achieved_gbs = nbytes / (attn_ms * 1e-3) / 1e9
     achieved_tfs = flops / (attn_ms * 1e-3) / 1e12
-    # counters were taken with the planner's default row path only
-    traffic = measured_traffic(b.name) if row_path == 0 else None
+    # counters were taken with the planner's default paths only
+    traffic = measured_traffic(b.name) if row_path == 0 and tile_path == 0 else None
+    # the matrix peak of the prefill work: bf16, or with fp8 score products
+    # half of the flops (Q K^T) at the fp8 peak and half (P V) at the bf16 one
+    mfma_peak = (MFMA_BF16_PEAK_TFS if tile_path != 2 else
+                 2.0 / (1.0 / MFMA_FP8_PEAK_TFS + 1.0 / MFMA_BF16_PEAK_TFS))
     # the batch is bound by whichever roof its algorithmic work reaches first
-    if flops / (MFMA_BF16_PEAK_TFS * 1e12) > nbytes / (HBM_PEAK_GBS * 1e9):
-        roof = {"bound": "mfma", "achieved": round(achieved_tfs, 1), "peak": MFMA_BF16_PEAK_TFS,
-                "unit": "TFLOP/s", "frac": round(achieved_tfs / MFMA_BF16_PEAK_TFS, 4),
+    if flops / (mfma_peak * 1e12) > nbytes / (HBM_PEAK_GBS * 1e9):
+        roof = {"bound": "mfma", "achieved": round(achieved_tfs, 1), "peak": round(mfma_peak, 1),
+                "unit": "TFLOP/s", "frac": round(achieved_tfs / mfma_peak, 4),
                 "traffic": traffic, "hbm_gbs": round(achieved_gbs, 1)}
+        if tile_path == 2:
+            roof["peak_note"] = "Q K^T at the fp8 MFMA peak, P V at the bf16 one (half of the flops each)"
+            roof["frac_of_bf16_peak"] = round(achieved_tfs / MFMA_BF16_PEAK_TFS, 4)
     else:
         roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": traffic}
@@ -670,7 +682,8 @@ def run_workload(name: str, args, log, full: bool = True, row_path: int = 0) -> 
                    "context_tokens": int(b.ctx_len.sum()), "q_heads": b.num_q_heads,
                    "kv_heads": b.num_kv_heads, "head_dim": b.head_dim, "block_size": 16,
                    "kv_split_tokens": int(info.kv_split_tokens), "seed": args.seed, "pool_copies": n_copies,
-                   "row_path": {1: "vector ALU", 2: "MFMA"}[int(info.row_path)]},
+                   "row_path": {1: "vector ALU", 2: "MFMA"}[int(info.row_path)],
+                   "tile_path": {1: "bf16", 2: "fp8 scores (opt-in)"}[int(info.tile_path)]},
         "roofline": roof,
     }
     app_ms = np.array([a.elapsed_time(c) for a, c in ev_append])
@@ -705,6 +718,8 @@ def main():
                          "with its own roofline under 'workloads' (default for mixed-8b: " +
                          ",".join(DEFAULT_ALSO) + "; 'none' for no others)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--tile-path", choices=("auto", "fp8qk"), default="auto",
+                    help="fp8qk: the prefill tiles' score products on fp8 MFMAs (opt-in arithmetic)")
     ap.add_argument("--row-path", choices=("auto", "valu"), default="auto",
                     help="where the main workload's row items run: the planner's choice (MFMA for eight query "
                          "heads per KV head) or the vector ALUs")
@@ -741,7 +756,8 @@ def main():
     if args.workload == "budget-sweep-fp8":
         budget_sweep(args, log)
         return
-    result = run_workload(args.workload, args, log, full=True, row_path=1 if args.row_path == "valu" else 0)
+    result = run_workload(args.workload, args, log, full=True, row_path=1 if args.row_path == "valu" else 0,
+                          tile_path=2 if args.tile_path == "fp8qk" else 0)
     if args.also is None:
         also = list(DEFAULT_ALSO) if args.workload == "mixed-8b" else []
     else:
@@ -750,13 +766,13 @@ def main():
         result["workloads"] = {}
     for entry in also:
         name, _, path = entry.partition("@")
-        if name not in WORKLOADS or name == "budget-sweep-fp8" or entry == args.workload or path not in ("", "valu"):
+        if name not in WORKLOADS or name == "budget-sweep-fp8" or entry == args.workload or path not in PATHS:
             raise SystemExit(f"--also: {entry} is not a single-batch workload other than the main one")
         gc.collect()
         torch.cuda.empty_cache()
-        sub = run_workload(name, args, log, full=False, row_path=1 if path == "valu" else 0)
+        sub = run_workload(name, args, log, full=False, row_path=PATHS[path][0], tile_path=PATHS[path][1])
         keep = ("value", "unit", "steps", "warmup", "ms_per_step", "dtype", "config", "roofline", "kv_append")
-        key = sub["config"]["workload"] + (" (vector-ALU rows)" if path == "valu" else "")
+        key = sub["config"]["workload"] + {"": "", "valu": " (vector-ALU rows)", "fp8qk": " (fp8 scores)"}[path]
         result["workloads"][key] = {k: sub[k] for k in keep}
         log(f"{name}: {sub['value']:.0f} query-tokens/s, {sub['roofline']['unit']} frac "
             f"{sub['roofline']['frac']}")

@@ -144,6 +144,7 @@ typedef struct {
   int32_t kv_dtype;
   int32_t out_dtype;
   int32_t row_path;          /* aug_row_path the plan's row items run on (VALU or MFMA, resolved) */
+  int32_t tile_path;         /* aug_tile_path the plan's prefill tiles run on (resolved) */
 } aug_attn_plan_info;
 
 /* Where the row items (decode rows) of a plan run. Groups of eight query
@@ -153,11 +154,23 @@ typedef struct {
  * MFMA where it can, VALU otherwise. */
 typedef enum { AUG_ROWS_AUTO = 0, AUG_ROWS_VALU = 1, AUG_ROWS_MFMA = 2 } aug_row_path;
 
+/* Arithmetic of the prefill tiles' score products S = Q K^T. BF16: Q and
+ * the (converted) keys as bf16 on 32x32x16 MFMAs, the default. FP8_QK, for
+ * fp8 KV with bf16 Q and head_dim 128 only: the keys stay fp8 and each query
+ * row is rounded to E4M3 with its own scale (largest magnitude / 448), on
+ * 32x32x64 fp8 MFMAs at twice the rate; P V stays bf16. Rounding Q to 3
+ * mantissa bits moves a logit by about 2^-5 of |q| |k| sqrt(head_dim) times
+ * the softmax scale, so outputs stay within the bf16 tolerances for
+ * near-uniform attention (keys of norm about 1) but not for sharp attention
+ * (keys of norm about sqrt(head_dim)): opt-in, never chosen by AUTO. */
+typedef enum { AUG_TILES_AUTO = 0, AUG_TILES_BF16 = 1, AUG_TILES_FP8_QK = 2 } aug_tile_path;
+
 /* Planner options (aug_attn_plan_opts). */
 typedef struct {
   int32_t kv_split_tokens;   /* as the argument of aug_attn_plan */
   int32_t row_path;          /* aug_row_path */
-  int32_t reserved[2];       /* zero */
+  int32_t tile_path;         /* aug_tile_path */
+  int32_t reserved;          /* zero */
 } aug_plan_options;
 
 /* Validate a formed batch and write its work list ("plan image") to
@@ -179,11 +192,12 @@ aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batc
                          int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
                          aug_attn_plan_info* info);
 
-/* aug_attn_plan with options: opts->kv_split_tokens as above, and the path
- * the row items run on (info->row_path records the resolved choice, which
- * aug_attn_mixed follows). Same image layout and errors, plus
- * AUG_ERR_UNSUPPORTED for AUG_ROWS_MFMA on a shape without that path and
- * AUG_ERR_INVALID for an unknown row path or non-zero reserved fields. */
+/* aug_attn_plan with options: opts->kv_split_tokens as above, the path the
+ * row items run on and the arithmetic of the prefill tiles (info->row_path
+ * and info->tile_path record the resolved choices, which aug_attn_mixed
+ * follows). Same image layout and errors, plus AUG_ERR_UNSUPPORTED for
+ * AUG_ROWS_MFMA or AUG_TILES_FP8_QK on a shape without that path and
+ * AUG_ERR_INVALID for an unknown path or a non-zero reserved field. */
 aug_status aug_attn_plan_opts(const aug_attn_shape* shape, const aug_batch_desc* batch,
                               const aug_plan_options* opts, void* plan_host, size_t plan_cap,
                               aug_attn_plan_info* info);

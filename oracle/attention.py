@@ -26,7 +26,7 @@ from typing import Iterable, Optional
 
 import numpy as np
 
-from .codecs import storage_to_f64
+from .codecs import e4m3fn_bits_to_f64, e4m3fn_encode, storage_to_f64
 
 BLOCK = 16
 
@@ -63,11 +63,35 @@ def attend_request(q_rows: np.ndarray, k: np.ndarray, v: np.ndarray, num_q_heads
     return out
 
 
+def round_query_rows_e4m3(q_rows: np.ndarray) -> np.ndarray:
+    """Query vectors as an fp8 score product sees them. This is not the
+    paper's arithmetic but an opt-in arithmetic of the kernel for prefill
+    chunks over an fp8 cache, defined here so that it can be checked: each
+    (row, head) vector of head_dim values is divided by its scale, the
+    largest magnitude over 448, rounded to the nearest E4M3FN value (ties to
+    even) and multiplied back by the scale. The scale and its reciprocal are
+    float32 values (reciprocal = 448 / largest magnitude, correctly rounded;
+    scale = largest magnitude times float32(1/448)), and the division is a
+    float32 product with the reciprocal, as the kernel computes them; an
+    all-zero vector stays zero. q_rows [n, H, D] float64 (bf16 values)."""
+    q32 = np.asarray(q_rows, dtype=np.float32)
+    amax = np.abs(q32).max(axis=-1, keepdims=True)
+    zero = amax == 0
+    inv = np.where(zero, np.float32(1.0), np.float32(448.0) / np.where(zero, np.float32(1.0), amax))
+    scale = np.where(zero, np.float32(1.0), amax * np.float32(1.0 / 448.0)).astype(np.float32)
+    x = (q32 * inv.astype(np.float32)).astype(np.float32)
+    codes = e4m3fn_encode(x)
+    return e4m3fn_bits_to_f64(codes) * scale.astype(np.float64)
+
+
 def paged_attention(q, q_dtype, k_cache, v_cache, k_scale, v_scale, kv_dtype,
                     q_start, ctx_len, bt_start, block_ids, num_q_heads, num_kv_heads,
-                    softmax_scale, requests: Optional[Iterable[int]] = None) -> np.ndarray:
+                    softmax_scale, requests: Optional[Iterable[int]] = None,
+                    fp8_chunk_queries: bool = False) -> np.ndarray:
     """Output rows [sum_q, H_q, D] float64. With ``requests`` given, only those
-    requests' rows are computed and every other row is NaN."""
+    requests' rows are computed and every other row is NaN. With
+    ``fp8_chunk_queries`` the query rows of every request with more than one
+    row (a prefill chunk) pass through ``round_query_rows_e4m3`` first."""
     total_q = int(q_start[-1])
     d = q.shape[-1]
     out = np.full((total_q, num_q_heads, d), np.nan, dtype=np.float64)
@@ -80,11 +104,14 @@ def paged_attention(q, q_dtype, k_cache, v_cache, k_scale, v_scale, kv_dtype,
         k = materialise_kv(k_cache, k_scale, kv_dtype, blocks, ctx)
         v = materialise_kv(v_cache, v_scale, kv_dtype, blocks, ctx)
         q_rows = storage_to_f64(q[q0:q1], q_dtype)
+        if fp8_chunk_queries and q1 - q0 > 1:
+            q_rows = round_query_rows_e4m3(q_rows)
         out[q0:q1] = attend_request(q_rows, k, v, num_q_heads, num_kv_heads, softmax_scale)
     return out
 
 
-def attention_for(batch, requests=None, k_cache=None, v_cache=None, k_scale=None, v_scale=None):
+def attention_for(batch, requests=None, k_cache=None, v_cache=None, k_scale=None, v_scale=None,
+                  fp8_chunk_queries=False):
     """Run ``paged_attention`` on a batch object carrying the standard fields;
     the cache arguments override the batch's own pool (e.g. after a resume)."""
     return paged_attention(
@@ -94,4 +121,4 @@ def attention_for(batch, requests=None, k_cache=None, v_cache=None, k_scale=None
         batch.k_scale if k_scale is None else k_scale,
         batch.v_scale if v_scale is None else v_scale,
         batch.kv_dtype, batch.q_start, batch.ctx_len, batch.bt_start, batch.block_ids,
-        batch.num_q_heads, batch.num_kv_heads, batch.softmax_scale, requests)
+        batch.num_q_heads, batch.num_kv_heads, batch.softmax_scale, requests, fp8_chunk_queries)

@@ -32,6 +32,7 @@ AUG_F32, AUG_BF16, AUG_FP8_E4M3FN = 0, 1, 2
 AUG_WAITING, AUG_RUNNING, AUG_SWAPPED, AUG_PAUSED = 0, 1, 2, 3
 AUG_POL_NONE, AUG_PRESERVE, AUG_DISCARD, AUG_SWAP = 0, 1, 2, 3
 AUG_ROWS_AUTO, AUG_ROWS_VALU, AUG_ROWS_MFMA = 0, 1, 2
+AUG_TILES_AUTO, AUG_TILES_BF16, AUG_TILES_FP8_QK = 0, 1, 2
 
 DTYPE_CODES = {"f32": AUG_F32, "bf16": AUG_BF16, "fp8": AUG_FP8_E4M3FN}
 
@@ -70,11 +71,12 @@ class aug_attn_plan_info(C.Structure):
                 ("num_tile_merge_groups", C.c_int32), ("num_append_items", C.c_int32),
                 ("num_q_heads", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
                 ("q_dtype", C.c_int32), ("kv_dtype", C.c_int32), ("out_dtype", C.c_int32),
-                ("row_path", C.c_int32)]
+                ("row_path", C.c_int32), ("tile_path", C.c_int32)]
 
 
 class aug_plan_options(C.Structure):
-    _fields_ = [("kv_split_tokens", C.c_int32), ("row_path", C.c_int32), ("reserved", C.c_int32 * 2)]
+    _fields_ = [("kv_split_tokens", C.c_int32), ("row_path", C.c_int32), ("tile_path", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class aug_request(C.Structure):
@@ -252,20 +254,21 @@ def _batch_desc(q_start, ctx_len, bt_start, num_pool_blocks, block_ids=None):
 
 
 def aug_attn_plan(shape: aug_attn_shape, q_start, ctx_len, bt_start, num_pool_blocks: int,
-                  block_ids=None, kv_split_tokens: int = 0, row_path: int = AUG_ROWS_AUTO):
+                  block_ids=None, kv_split_tokens: int = 0, row_path: int = AUG_ROWS_AUTO,
+                  tile_path: int = AUG_TILES_AUTO):
     """Validate a batch (host arrays) and build its plan image (aug_attn_plan,
-    or aug_attn_plan_opts when a row path is requested). Returns (info, plan)
-    with plan a numpy uint8 array of info.plan_bytes bytes."""
+    or aug_attn_plan_opts when a row or tile path is requested). Returns
+    (info, plan) with plan a numpy uint8 array of info.plan_bytes bytes."""
     L = lib()
     desc, keep = _batch_desc(q_start, ctx_len, bt_start, num_pool_blocks, block_ids)
-    opts = aug_plan_options(int(kv_split_tokens), int(row_path))
+    opts = aug_plan_options(int(kv_split_tokens), int(row_path), int(tile_path))
     info = aug_attn_plan_info()
     # one scratch image per thread: ctypes releases the GIL during the call
     buf = getattr(_plan_scratch, "buf", None)
     if buf is None:
         buf = _plan_scratch.buf = np.zeros(1 << 20, dtype=np.uint8)
     while True:
-        if row_path == AUG_ROWS_AUTO:
+        if row_path == AUG_ROWS_AUTO and tile_path == AUG_TILES_AUTO:
             st = L.aug_attn_plan(C.byref(shape), C.byref(desc), int(kv_split_tokens), buf.ctypes.data,
                                  buf.nbytes, C.byref(info))
         else:

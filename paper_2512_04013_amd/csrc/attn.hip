@@ -58,6 +58,7 @@ using aug::WorkItem;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef int v8i_t __attribute__((ext_vector_type(8)));   // 32 fp8 codes: one 32x32x64 MFMA operand
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegBig = -1.0e30f;   // finite "minus infinity" for running maxima
@@ -866,6 +867,7 @@ __device__ void row_item_mfma(const WorkItem& it, const AttnArgs& a, float* lds)
 template <int D>
 struct TileLds {
   static constexpr int KS = D + 8;    // K row stride (elements): 16-byte aligned, conflict-free reads
+  static constexpr int KS8 = D + 16;  // K row stride (bytes) of fp8 keys kept as codes
   // V row stride (elements): rows 64 bytes apart modulo the 256-byte bank
   // width, so the transposing reads of four consecutive rows hit distinct banks
   static constexpr int VS = D + 32;
@@ -929,12 +931,13 @@ template <bool B> using bool_tag = std::integral_constant<bool, B>;
 // Tiles that every row reads in full (all keys at or below the first row's
 // position and inside the span, all block ids inside the pool) take a path
 // without per-key conditions; only the diagonal and span-end tiles mask.
-template <int KVT, int D, int G, int OT>
+template <int KVT, int D, int G, int OT, bool QK8>
 __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* smem) {
   using L = TileLds<D>;
   using TS = TileStage<KVT>;
   using raw_t = typename TS::raw_t;
   constexpr bool FP8 = KVT == KV_FP8;
+  static_assert(!QK8 || (FP8 && D == 128), "fp8 score products need fp8 keys and head_dim 128");
   constexpr int EB = FP8 ? 1 : 2;     // bytes per K/V element
   constexpr int KSTEPS = D / 16;      // k-steps of S^T over head_dim
   constexpr int DB = D / 32;          // 32-dim blocks of O^T
@@ -957,12 +960,58 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   // (and +8) of a 16-key step at dimension m of a 32-dim block
   const int v_lane_off = (4 * hh + (lane & 15) / 4) * L::VS + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  uint4 qreg[KSTEPS];
+  // bf16 scores: Q^T operands of the KSTEPS k-steps, dims 16s + 8hh .. + 7.
+  // fp8 scores: the row rounded to E4M3 after division by its scale qscale
+  // (largest magnitude / 448), as the B operands of the two 64-dim k-steps:
+  // lane half hh holds dims 64h + 32hh .. + 31 of k-step h.
+  uint4 qreg[QK8 ? 1 : KSTEPS];
+  v8i_t q8[2];
+  float qscale = 1.f;
   {
     const int64_t qoff = (static_cast<int64_t>(it.q_row0 + p) * a.hq + static_cast<int64_t>(kvh) * G + gh) * D;
+    if constexpr (!QK8) {
 #pragma unroll
-    for (int s = 0; s < KSTEPS; ++s)
-      qreg[s] = row_ok ? *reinterpret_cast<const uint4*>(qb + qoff + 16 * s + 8 * hh) : uint4{0, 0, 0, 0};
+      for (int s = 0; s < KSTEPS; ++s)
+        qreg[s] = row_ok ? *reinterpret_cast<const uint4*>(qb + qoff + 16 * s + 8 * hh) : uint4{0, 0, 0, 0};
+    } else {
+      uint4 raw[2][4];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4)
+          raw[h][c4] = row_ok ? *reinterpret_cast<const uint4*>(qb + qoff + 64 * h + 32 * hh + 8 * c4)
+                              : uint4{0, 0, 0, 0};
+      float amax = 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4) {
+          const uint32_t w[4] = {raw[h][c4].x, raw[h][c4].y, raw[h][c4].z, raw[h][c4].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            amax = fmaxf(amax, fmaxf(fabsf(__uint_as_float(w[e] << 16)), fabsf(__uint_as_float(w[e] & 0xFFFF0000u))));
+        }
+      amax = max_across_halves(amax);
+      qscale = amax > 0.f ? amax * (1.f / 448.f) : 1.f;
+      const float inv = amax > 0.f ? 448.f / amax : 1.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4) {
+          const uint32_t w[4] = {raw[h][c4].x, raw[h][c4].y, raw[h][c4].z, raw[h][c4].w};
+          // eight dims -> two dwords of four E4M3 codes (dim order kept)
+          int lo = __builtin_amdgcn_cvt_pk_fp8_f32(__uint_as_float(w[0] << 16) * inv,
+                                                  __uint_as_float(w[0] & 0xFFFF0000u) * inv, 0, false);
+          lo = __builtin_amdgcn_cvt_pk_fp8_f32(__uint_as_float(w[1] << 16) * inv,
+                                              __uint_as_float(w[1] & 0xFFFF0000u) * inv, lo, true);
+          int hi = __builtin_amdgcn_cvt_pk_fp8_f32(__uint_as_float(w[2] << 16) * inv,
+                                                  __uint_as_float(w[2] & 0xFFFF0000u) * inv, 0, false);
+          hi = __builtin_amdgcn_cvt_pk_fp8_f32(__uint_as_float(w[3] << 16) * inv,
+                                              __uint_as_float(w[3] & 0xFFFF0000u) * inv, hi, true);
+          q8[h][2 * c4] = lo;
+          q8[h][2 * c4 + 1] = hi;
+        }
+    }
   }
 
   f32x16_t acc_o[DB];
@@ -1043,7 +1092,12 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     uint16_t* vs = ks + 64 * L::KS;
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
-      *reinterpret_cast<uint4*>(ks + (tk * KPT + u) * L::KS + 8 * tc) = TS::to_bf16(kr[u]);
+      if constexpr (QK8) {
+        // keys stay fp8: rows of KS8 bytes
+        *reinterpret_cast<raw_t*>(reinterpret_cast<unsigned char*>(ks) + (tk * KPT + u) * L::KS8 + 8 * tc) = kr[u];
+      } else {
+        *reinterpret_cast<uint4*>(ks + (tk * KPT + u) * L::KS + 8 * tc) = TS::to_bf16(kr[u]);
+      }
       *reinterpret_cast<uint4*>(vs + (tk * KPT + u) * L::VS + 8 * tc) = TS::to_bf16(vr[u]);
     }
     if constexpr (FP8) {
@@ -1080,7 +1134,33 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     // S^T = K Q^T for keys k0..k0+63. All K operands of the tile are read
     // from LDS first, so the reads stream while the MFMAs consume them in order.
     f32x16_t sacc[2];
-    {
+    if constexpr (QK8) {
+      // fp8: K rows of 128 codes against the rounded Q, two 64-dim k-steps
+      // per 32 keys on 32x32x64 fp8 MFMAs (unit block scales)
+      const unsigned char* k8 = reinterpret_cast<const unsigned char*>(ks);
+      v8i_t kop[2][2];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const unsigned char* src = k8 + (32 * mb + n) * L::KS8 + 64 * h + 32 * hh;
+          const uint4 lo = *reinterpret_cast<const uint4*>(src);
+          const uint4 hi = *reinterpret_cast<const uint4*>(src + 16);
+          kop[mb][h] = v8i_t{static_cast<int>(lo.x), static_cast<int>(lo.y), static_cast<int>(lo.z),
+                             static_cast<int>(lo.w), static_cast<int>(hi.x), static_cast<int>(hi.y),
+                             static_cast<int>(hi.z), static_cast<int>(hi.w)};
+        }
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(0);
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sacc[mb][e] = 0.f;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          sacc[mb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kop[mb][h], q8[h], sacc[mb], 0, 0, 0, 127, 0, 127);
+      }
+    } else {
       uint4 kop[2][KSTEPS];
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
@@ -1133,7 +1213,7 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     float coef[4], vlog[4], vinv[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
-      coef[b] = FP8 ? stage_scales[stage * L::NSC + b] : c;
+      coef[b] = FP8 ? stage_scales[stage * L::NSC + b] * (QK8 ? qscale : 1.f) : c;
       vlog[b] = FP8 ? stage_scales[stage * L::NSC + 4 + b] : 0.f;
       vinv[b] = FP8 ? stage_scales[stage * L::NSC + 8 + b] : 1.f;
     }
@@ -1263,7 +1343,7 @@ constexpr bool row_mfma_capable() {
   return G == 8 && D == 128 && (KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16;
 }
 
-template <int KVT, int D, int G, int QT, int OT, bool TILES, bool ROW_MFMA, int NW>
+template <int KVT, int D, int G, int QT, int OT, bool TILES, bool ROW_MFMA, int NW, bool QK8 = false>
 __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   static_assert(!TILES || NW == kThreads / 64, "tile items run on four-wave workgroups");
   constexpr int RB = row_lds_bytes<D, G, NW>();
@@ -1274,7 +1354,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   const WorkItem it = a.items[blockIdx.x];
   if constexpr (TILES) {
     if (it.kind == aug::kTileItem) {
-      tile_item<KVT, D, G, OT>(it, a, smem);
+      tile_item<KVT, D, G, OT, QK8>(it, a, smem);
       return;
     }
   }
@@ -1295,9 +1375,9 @@ __global__ __launch_bounds__(64 * NW) void attn_rows_kernel(AttnArgs a) {
 // Mixed batches: MFMA tiles and row items in one launch. The tile path's
 // accumulators set the register budget (two waves per SIMD); the row path
 // spends the same budget on prefetching the next block.
-template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
+template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA, bool QK8>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mixed_kernel(AttnArgs a) {
-  attn_body<KVT, D, G, QT, OT, true, ROW_MFMA, kThreads / 64>(a);
+  attn_body<KVT, D, G, QT, OT, true, ROW_MFMA, kThreads / 64, QK8>(a);
 }
 
 // Merge launch for split prefill tiles: one workgroup per (row, KV head)
@@ -1312,8 +1392,17 @@ template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
 aug_status launch_rows(const AttnArgs& a, const aug_attn_plan_info& info, hipStream_t st) {
   if (info.num_prefill_items > 0) {
     if constexpr ((KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16) {
-      hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA>), dim3(info.num_items), dim3(kThreads), 0,
-                         st, a);
+      if (info.tile_path == AUG_TILES_FP8_QK) {
+        if constexpr (KVT == KV_FP8 && D == 128) {
+          hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA, true>), dim3(info.num_items),
+                             dim3(kThreads), 0, st, a);
+        } else {
+          return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: fp8 score products need fp8 KV and head_dim 128");
+        }
+      } else {
+        hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA, false>), dim3(info.num_items),
+                           dim3(kThreads), 0, st, a);
+      }
     } else {
       return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: plan has tiles for a dtype set without them");
     }

@@ -41,6 +41,11 @@ bool tiles_supported(const aug_attn_shape& s) {
   return s.q_dtype == AUG_BF16 && (s.kv_dtype == AUG_BF16 || s.kv_dtype == AUG_FP8_E4M3FN);
 }
 
+// fp8 score products on the tiles: fp8 keys (head_dim 128) and bf16 queries
+bool tile_fp8qk_supported(const aug_attn_shape& s) {
+  return s.q_dtype == AUG_BF16 && s.kv_dtype == AUG_FP8_E4M3FN && s.head_dim == 128;
+}
+
 aug_status check_shape(const aug_attn_shape* s, const char* who) {
   if (!s) return fail(AUG_ERR_INVALID, "%s: shape is NULL", who);
   if (s->num_q_heads < 1 || s->num_kv_heads < 1 || s->num_q_heads % s->num_kv_heads != 0)
@@ -84,6 +89,9 @@ aug_status check_plan_info(const aug_attn_plan_info* info, const aug_attn_shape*
                 s->out_dtype);
   if (info->row_path != AUG_ROWS_VALU && !(info->row_path == AUG_ROWS_MFMA && row_mfma_supported(*s)))
     return fail(AUG_ERR_INVALID, "%s: info names row path %d, which this shape cannot run", who, info->row_path);
+  if (info->tile_path != AUG_TILES_BF16 && !(info->tile_path == AUG_TILES_FP8_QK && tile_fp8qk_supported(*s)))
+    return fail(AUG_ERR_INVALID, "%s: info names tile path %d, which this shape cannot run", who,
+                info->tile_path);
   return AUG_OK;
 }
 
@@ -140,7 +148,7 @@ using namespace aug;
 extern "C" aug_status aug_attn_plan(const aug_attn_shape* s, const aug_batch_desc* b,
                                     int32_t kv_split_tokens, void* plan_host, size_t plan_cap,
                                     aug_attn_plan_info* info) {
-  const aug_plan_options opts{kv_split_tokens, AUG_ROWS_AUTO, {0, 0}};
+  const aug_plan_options opts{kv_split_tokens, AUG_ROWS_AUTO, AUG_TILES_AUTO, 0};
   return aug_attn_plan_opts(s, b, &opts, plan_host, plan_cap, info);
 }
 
@@ -150,8 +158,7 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
   const char* who = "aug_attn_plan";
   if (aug_status st = check_shape(s, who); st != AUG_OK) return st;
   if (!opts) return fail(AUG_ERR_INVALID, "%s: options are NULL", who);
-  if (opts->reserved[0] != 0 || opts->reserved[1] != 0)
-    return fail(AUG_ERR_INVALID, "%s: reserved option fields must be zero", who);
+  if (opts->reserved != 0) return fail(AUG_ERR_INVALID, "%s: the reserved option field must be zero", who);
   const int32_t kv_split_tokens = opts->kv_split_tokens;
   int32_t row_path = opts->row_path;
   if (row_path != AUG_ROWS_AUTO && row_path != AUG_ROWS_VALU && row_path != AUG_ROWS_MFMA)
@@ -160,6 +167,12 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
     return fail(AUG_ERR_UNSUPPORTED, "%s: the MFMA row path needs 8 query heads per KV head, head_dim 128 and "
                 "bf16 or fp8 KV", who);
   if (row_path == AUG_ROWS_AUTO) row_path = row_mfma_supported(*s) ? AUG_ROWS_MFMA : AUG_ROWS_VALU;
+  int32_t tile_path = opts->tile_path;
+  if (tile_path != AUG_TILES_AUTO && tile_path != AUG_TILES_BF16 && tile_path != AUG_TILES_FP8_QK)
+    return fail(AUG_ERR_INVALID, "%s: unknown tile path %d", who, tile_path);
+  if (tile_path == AUG_TILES_FP8_QK && !tile_fp8qk_supported(*s))
+    return fail(AUG_ERR_UNSUPPORTED, "%s: fp8 score products need fp8 KV, bf16 queries and head_dim 128", who);
+  if (tile_path == AUG_TILES_AUTO) tile_path = AUG_TILES_BF16;   // fp8 scores are opt-in
   if (!b || !info) return fail(AUG_ERR_INVALID, "%s: batch or info is NULL", who);
   const int32_t n = b->num_reqs;
   if (n < 0) return fail(AUG_ERR_INVALID, "%s: num_reqs %d < 0", who, n);
@@ -404,6 +417,7 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
   info->kv_dtype = s->kv_dtype;
   info->out_dtype = s->out_dtype;
   info->row_path = row_path;
+  info->tile_path = tile_path;
   if (!plan_host) return AUG_OK;
   if (plan_cap < static_cast<size_t>(plan_bytes))
     return fail(AUG_ERR_NO_SPACE, "%s: plan buffer %zu < %lld bytes", who, plan_cap,
@@ -431,6 +445,7 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
   hdr.kv_dtype = static_cast<int8_t>(s->kv_dtype);
   hdr.out_dtype = static_cast<int8_t>(s->out_dtype);
   hdr.row_path = static_cast<int8_t>(row_path);
+  hdr.tile_path = static_cast<int8_t>(tile_path);
   std::memcpy(base, &hdr, sizeof(hdr));
   auto* items = reinterpret_cast<WorkItem*>(base + items_off);
   auto* groups = reinterpret_cast<MergeGroup*>(base + groups_off);

@@ -7,7 +7,7 @@
 namespace aug {
 
 constexpr int32_t kPlanMagic = 0x4E4C5041;  // "APLN"
-constexpr int32_t kPlanVersion = 3;
+constexpr int32_t kPlanVersion = 4;
 constexpr int32_t kBlock = 16;              // tokens per KV block
 constexpr int32_t kKeyTile = 64;            // keys per MFMA tile (4 blocks)
 constexpr int32_t kTileRows = 128;          // query rows (positions x group heads) per MFMA tile
@@ -43,7 +43,8 @@ struct PlanHeader {          // 64 bytes
   int8_t kv_dtype;
   int8_t out_dtype;
   int8_t row_path;           // aug_row_path of the row items (resolved)
-  int16_t reserved1;
+  int8_t tile_path;          // aug_tile_path of the prefill tiles (resolved)
+  int8_t reserved1;
 };
 
 struct WorkItem {            // 48 bytes

@@ -63,12 +63,13 @@ class MixedAttention:
 
     def __init__(self, shape, kv: PagedKV, q_start, ctx_len, bt_start, block_ids_host,
                  block_ids_dev: torch.Tensor, kv_split_tokens: int = 0, check_blocks: bool = True,
-                 row_path: int = 0):
+                 row_path: int = 0, tile_path: int = 0):
         self.shape, self.kv = shape, kv
         device = kv.k_cache.device
         self.info, plan = aug_attn_plan(shape, q_start, ctx_len, bt_start, kv.num_pool_blocks,
                                         block_ids_host if check_blocks else None,
-                                        kv_split_tokens=kv_split_tokens, row_path=row_path)
+                                        kv_split_tokens=kv_split_tokens, row_path=row_path,
+                                        tile_path=tile_path)
         # pinned staging kept alive with the batch; the library's copy kernel
         # moves it on the current stream of the cache's device
         self.plan_host = torch.from_numpy(plan.copy()).pin_memory()

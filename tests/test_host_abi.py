@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol():
     L = aug.lib()
     for name in declared:
         assert hasattr(L, name), name
-    assert aug.aug_abi_version() >> 16 == 2
+    assert aug.aug_abi_version() >> 16 == 3
     assert aug.aug_status_string(aug.AUG_ERR_NO_SPACE) == "AUG_ERR_NO_SPACE"
 
 
@@ -37,7 +37,7 @@ def _shape(b):
 
 def _decode_plan(plan):
     hdr = plan[:64].view(np.int32)
-    assert hdr[0] == 0x4E4C5041 and hdr[1] == 3
+    assert hdr[0] == 0x4E4C5041 and hdr[1] == 4
     n_items, n_groups = hdr[2], hdr[4]
     item_t = np.dtype([("kvh", "<i2"), ("kind", "i1"), ("res", "i1"), ("q_row0", "<i4"),
                        ("n_rows", "<i2"), ("stride", "<i2"), ("kb", "<i4"), ("ke", "<i4"),
@@ -330,7 +330,7 @@ def test_row_path_option_resolves_and_is_checked():
     assert e.value.status == aug.AUG_ERR_INVALID
     desc, keep = aug._batch_desc(q_start, ctx, bt_start, pool)
     opts = aug.aug_plan_options(0, 0)
-    opts.reserved[1] = 3
+    opts.reserved = 3
     out = aug.aug_attn_plan_info()
     assert L.aug_attn_plan_opts(aug.C.byref(g8), aug.C.byref(desc), aug.C.byref(opts), None, 0,
                                 aug.C.byref(out)) == aug.AUG_ERR_INVALID
@@ -361,6 +361,35 @@ def test_default_split_doubles_for_mfma_rows_without_tiles():
     assert plan(g8, [1] * 20, small, kv_split_tokens=300).kv_split_tokens == 304
     g4 = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)
     assert plan(g4, [1] * 20, small).kv_split_tokens == 512
+
+
+def test_tile_path_option_resolves_and_is_checked():
+    """fp8 score products on the tiles are opt-in: AUTO resolves to bf16; FP8_QK
+    is accepted for fp8 KV with bf16 queries (head_dim 128) and refused for
+    other dtype sets; the resolved path is in the info and the plan header,
+    and a call refuses an info naming a path its shape lacks."""
+    L = aug.lib()
+    q_start, ctx = [0, 5, 6], [50, 20]
+    bt_start = np.concatenate([[0], np.cumsum([-(-c // 16) for c in ctx])])
+    pool = int(bt_start[-1]) + 4
+    f8 = aug.make_shape(16, 2, 128, "bf16", "fp8", "bf16", 0.088)
+    b16 = aug.make_shape(16, 2, 128, "bf16", "bf16", "bf16", 0.088)
+    info, plan = aug.aug_attn_plan(f8, q_start, ctx, bt_start, pool)
+    assert info.tile_path == aug.AUG_TILES_BF16 and plan[62] == aug.AUG_TILES_BF16
+    info, plan = aug.aug_attn_plan(f8, q_start, ctx, bt_start, pool, tile_path=aug.AUG_TILES_FP8_QK)
+    assert info.tile_path == aug.AUG_TILES_FP8_QK and plan[62] == aug.AUG_TILES_FP8_QK
+    info16, _ = aug.aug_attn_plan(b16, q_start, ctx, bt_start, pool, tile_path=aug.AUG_TILES_BF16)
+    assert info16.tile_path == aug.AUG_TILES_BF16
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_plan(b16, q_start, ctx, bt_start, pool, tile_path=aug.AUG_TILES_FP8_QK)
+    assert e.value.status == aug.AUG_ERR_UNSUPPORTED
+    with pytest.raises(AugError) as e:
+        aug.aug_attn_plan(f8, q_start, ctx, bt_start, pool, tile_path=9)
+    assert e.value.status == aug.AUG_ERR_INVALID
+    bad = aug.aug_attn_plan_info.from_buffer_copy(info16)
+    bad.tile_path = aug.AUG_TILES_FP8_QK
+    st = L.aug_attn_mixed(aug.C.byref(b16), aug.C.byref(bad), 8, 8, 8, 8, None, None, 8, pool, 8, 8, 1 << 40, None)
+    assert st == aug.AUG_ERR_INVALID and "tile path" in aug.aug_last_error()
 
 
 def test_noalloc_attention_rejects_bad_arguments_without_touching_the_gpu():

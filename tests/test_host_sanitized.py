@@ -22,7 +22,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 DEVICE_TESTS = ("exports_every", "park_and_attention", "kv_append_rejects", "plan_upload_rejects",
-                "shape_is_refused", "noalloc", "row_path_option", "empty_batches")
+                "shape_is_refused", "noalloc", "row_path_option", "tile_path_option", "empty_batches")
 
 
 def _asan_runtime():

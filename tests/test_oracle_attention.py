@@ -265,3 +265,63 @@ def test_resumed_batch_attention_equals_original_placement():
     assert np.isnan(oa.attention_for(b)).any()
     out = oa.attention_for(b, k_cache=k2, v_cache=v2)
     assert np.isfinite(out).all()
+
+
+# ---- queries rounded to E4M3 (the opt-in fp8 score arithmetic of prefill tiles) ----------
+
+def _nearest_by_search(x, scale):
+    """Brute force: the E4M3FN value times `scale` nearest to x (ties to the
+    even code), over all 254 finite codes, element by element."""
+    table = codecs.E4M3FN_TABLE
+    finite = [c for c in range(256) if np.isfinite(table[c])]
+    out = np.empty_like(x)
+    for i, xi in enumerate(x.ravel()):
+        best, best_d = None, None
+        for c in finite:
+            d = abs(table[c] * scale - xi)
+            if best is None or d < best_d or (d == best_d and (c & 1) == 0 and (best & 1) == 1):
+                best, best_d = c, d
+        out.ravel()[i] = table[best] * scale
+    return out
+
+
+def test_rounded_queries_on_the_grid_are_unchanged():
+    # a vector whose largest magnitude is 448 x 2^-5 and whose entries are all
+    # E4M3 values times 2^-5: scale 2^-5 exactly, so rounding changes nothing
+    rng = np.random.default_rng(0)
+    codes = rng.integers(0, 0x7F, size=(3, 2, 128)).astype(np.uint8)
+    vals = codecs.e4m3fn_bits_to_f64(codes) * np.where(rng.random((3, 2, 128)) < 0.5, -1, 1)
+    vals[..., 7] = 448.0
+    q = vals * 2.0 ** -5
+    np.testing.assert_array_equal(oa.round_query_rows_e4m3(q), q)
+
+
+def test_rounded_queries_are_the_nearest_scaled_e4m3_values():
+    rng = np.random.default_rng(1)
+    q = torch.from_numpy(rng.standard_normal((2, 2, 32))).to(torch.bfloat16).double().numpy()
+    got = oa.round_query_rows_e4m3(q)
+    for r in range(2):
+        for h in range(2):
+            amax = np.float32(np.abs(q[r, h]).max())
+            scale = float(amax * np.float32(1.0 / 448.0))
+            x = q[r, h].astype(np.float32) * (np.float32(448.0) / amax)
+            want = _nearest_by_search(x.astype(np.float64), 1.0) * scale
+            np.testing.assert_array_equal(got[r, h], want)
+    # relative error of 3 mantissa bits in the normal range, and the largest
+    # magnitude maps to 448 x scale (the vector's own maximum, up to rounding)
+    rel = np.abs(got - q) / np.maximum(np.abs(q), 1e-30)
+    normal = np.abs(q) >= np.abs(q).max(axis=-1, keepdims=True) * 2.0 ** -6 / 448   # E4M3 normals
+    assert (rel[normal] <= 2.0 ** -4 + 1e-7).all()
+    np.testing.assert_allclose(np.abs(got).max(axis=-1), np.abs(q).max(axis=-1), rtol=2e-7)
+
+
+def test_rounded_queries_zero_vector_and_chunk_rows_only():
+    assert (oa.round_query_rows_e4m3(np.zeros((1, 1, 16))) == 0).all()
+    b = make_batch_from_lengths("fp8q", [1, 5, 1], [40, 70, 33], num_q_heads=8, num_kv_heads=2,
+                                head_dim=128, q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16",
+                                n_pool_blocks=64, seed=5)
+    plain = oa.attention_for(b)
+    rounded = oa.attention_for(b, fp8_chunk_queries=True)
+    dec = np.r_[0, 6]                      # the two decode rows: untouched
+    np.testing.assert_array_equal(rounded[dec], plain[dec])
+    assert not np.array_equal(rounded[1:6], plain[1:6])
