@@ -1384,8 +1384,61 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 // group; the attention launch before it wrote the partials.
 template <int D, int G, int OT>
 __global__ __launch_bounds__(kThreads) void tile_merge_kernel(AttnArgs a) {
-  __shared__ float lds[merge_lds_floats(G)];
-  merge_group<D, G, OT, kThreads>(a.groups[blockIdx.x], a.partials, a.out, a.hq, lds);
+  // Every thread merges four consecutive output dims of one head on its own:
+  // it reads each span's (m, l) of that head and its four partial values,
+  // all independent loads, and folds them in online (log-sum-exp), so the
+  // group costs one memory round trip per eight spans and no barrier. The
+  // partials come from the previous launch, so plain loads see them.
+  const MergeGroup g = a.groups[blockIdx.x];
+  const int64_t pf = aug::partial_floats(G, D);
+  const float* base = a.partials + static_cast<int64_t>(g.part0) * pf;
+  for (int c = threadIdx.x; c < G * D / 4; c += kThreads) {
+    const int h = (4 * c) / D;
+    float mx = kNegBig, l = 0.f;
+    float4 o = {0.f, 0.f, 0.f, 0.f};
+    int s = 0;
+    for (; s + 8 <= g.n_parts; s += 8) {
+      float ms[8], ls[8];
+      float4 os[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float* p = base + static_cast<int64_t>(s + k) * pf;
+        ms[k] = p[G * D + h];
+        ls[k] = p[G * D + G + h];
+        os[k] = *reinterpret_cast<const float4*>(p + 4 * c);
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float mn = fmaxf(mx, ms[k]);
+        const float a0 = __builtin_amdgcn_exp2f(mx - mn), a1 = __builtin_amdgcn_exp2f(ms[k] - mn);
+        l = l * a0 + ls[k] * a1;
+        o.x = o.x * a0 + os[k].x * a1;
+        o.y = o.y * a0 + os[k].y * a1;
+        o.z = o.z * a0 + os[k].z * a1;
+        o.w = o.w * a0 + os[k].w * a1;
+        mx = mn;
+      }
+    }
+    for (; s < g.n_parts; ++s) {
+      const float* p = base + static_cast<int64_t>(s) * pf;
+      const float ms = p[G * D + h], ls = p[G * D + G + h];
+      const float4 os = *reinterpret_cast<const float4*>(p + 4 * c);
+      const float mn = fmaxf(mx, ms);
+      const float a0 = __builtin_amdgcn_exp2f(mx - mn), a1 = __builtin_amdgcn_exp2f(ms - mn);
+      l = l * a0 + ls * a1;
+      o.x = o.x * a0 + os.x * a1;
+      o.y = o.y * a0 + os.y * a1;
+      o.z = o.z * a0 + os.z * a1;
+      o.w = o.w * a0 + os.w * a1;
+      mx = mn;
+    }
+    const float inv = 1.f / l;
+    const int64_t off = (static_cast<int64_t>(g.q_row) * a.hq + static_cast<int64_t>(g.kvh) * G) * D + 4 * c;
+    store_out<OT>(a.out, off + 0, o.x * inv);
+    store_out<OT>(a.out, off + 1, o.y * inv);
+    store_out<OT>(a.out, off + 2, o.z * inv);
+    store_out<OT>(a.out, off + 3, o.w * inv);
+  }
 }
 
 template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
