@@ -257,83 +257,60 @@ __device__ __forceinline__ void store_partial(float* p, float v) {
 __device__ __forceinline__ float load_partial(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+__device__ __forceinline__ float2 load_partial2(const float* p) {
+  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  return float2{__uint_as_float(static_cast<uint32_t>(v)), __uint_as_float(static_cast<uint32_t>(v >> 32))};
+}
 
-// Merge the partials of one (row, KV head) group with a workgroup of NT
-// threads: O = sum_s o_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), M = max_s m_s.
-// The (m, l) pairs are staged in LDS (kMergeStage x 2G floats) so the output
-// loads of all partials are independent; the per-head running maximum, sum
-// and rescale factor follow them in LDS (3G floats), kept by threads 0..G-1.
-constexpr int kMergeStage = 64;   // partials staged per pass
-constexpr int merge_lds_floats(int g) { return kMergeStage * 2 * g + 3 * g; }
-
+// Merge of one (row, KV head) group without LDS or barriers: every thread
+// folds four output dims of one head over all spans online, its loads of
+// (m, l) and of the partial values all independent (device-scope loads,
+// since the partials come from other workgroups of this launch).
 template <int D, int G, int OT, int NT>
-__device__ __forceinline__ void merge_group(const MergeGroup& g, const float* partials, void* out, int32_t hq,
-                                            float* lds) {
-  static_assert(G <= NT, "one thread per head keeps the running statistics");
+__device__ __forceinline__ void merge_group_direct(const MergeGroup& g, const float* partials, void* out,
+                                                   int32_t hq) {
   const int64_t pf = aug::partial_floats(G, D);
-  constexpr int PER = (G * D + NT - 1) / NT;   // output elements per thread
-  float* ml = lds;
-  float* run_m = lds + kMergeStage * 2 * G;
-  float* run_l = run_m + G;
-  float* rescale = run_l + G;
-  float acc[PER];
+  const float* base = partials + static_cast<int64_t>(g.part0) * pf;
+  for (int c = threadIdx.x; c < G * D / 4; c += NT) {
+    const int h = (4 * c) / D;
+    float mx = kNegBig, l = 0.f, o0 = 0.f, o1 = 0.f, o2 = 0.f, o3 = 0.f;
+    int s = 0;
+    auto fold = [&](float ms, float ls, float2 x01, float2 x23) {
+      const float mn = fmaxf(mx, ms);
+      const float a0 = __builtin_amdgcn_exp2f(mx - mn), a1 = __builtin_amdgcn_exp2f(ms - mn);
+      l = l * a0 + ls * a1;
+      o0 = o0 * a0 + x01.x * a1;
+      o1 = o1 * a0 + x01.y * a1;
+      o2 = o2 * a0 + x23.x * a1;
+      o3 = o3 * a0 + x23.y * a1;
+      mx = mn;
+    };
+    for (; s + 4 <= g.n_parts; s += 4) {
+      float ms[4], ls[4];
+      float2 x01[4], x23[4];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) acc[k] = 0.f;
-  if (threadIdx.x < G) {
-    run_m[threadIdx.x] = kNegBig;
-    run_l[threadIdx.x] = 0.f;
-  }
-  for (int s0 = 0; s0 < g.n_parts; s0 += kMergeStage) {
-    const int ns = min(kMergeStage, g.n_parts - s0);
-    __syncthreads();
-    for (int i = threadIdx.x; i < ns * 2 * G; i += NT) {
-      const int s = i / (2 * G);
-      const int j = i % (2 * G);
-      ml[s * 2 * G + j] = load_partial(partials + (g.part0 + s0 + s) * pf + G * D + j);
-    }
-    __syncthreads();
-    if (threadIdx.x < G) {
-      // this pass's maximum for head h, and the rescaling of what earlier passes summed
-      const int h = threadIdx.x;
-      float m = run_m[h];
-      for (int s = 0; s < ns; ++s) m = fmaxf(m, ml[s * 2 * G + h]);
-      const float old = __builtin_amdgcn_exp2f(run_m[h] - m);
-      float l = run_l[h] * old;
-      for (int s = 0; s < ns; ++s) l += ml[s * 2 * G + G + h] * __builtin_amdgcn_exp2f(ml[s * 2 * G + h] - m);
-      run_m[h] = m;
-      run_l[h] = l;
-      rescale[h] = old;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int idx = threadIdx.x + k * NT;
-      if (idx >= G * D) break;
-      const int h = idx / D;
-      const float mh = run_m[h];
-      float o = acc[k] * rescale[h];
-      const float* base = partials + static_cast<int64_t>(g.part0 + s0) * pf + idx;
-      int s = 0;
-      for (; s + 4 <= ns; s += 4) {
-        const float o0 = load_partial(base + (s + 0) * pf), o1 = load_partial(base + (s + 1) * pf);
-        const float o2 = load_partial(base + (s + 2) * pf), o3 = load_partial(base + (s + 3) * pf);
-        o += o0 * __builtin_amdgcn_exp2f(ml[(s + 0) * 2 * G + h] - mh);
-        o += o1 * __builtin_amdgcn_exp2f(ml[(s + 1) * 2 * G + h] - mh);
-        o += o2 * __builtin_amdgcn_exp2f(ml[(s + 2) * 2 * G + h] - mh);
-        o += o3 * __builtin_amdgcn_exp2f(ml[(s + 3) * 2 * G + h] - mh);
+      for (int k = 0; k < 4; ++k) {
+        const float* p = base + static_cast<int64_t>(s + k) * pf;
+        ms[k] = load_partial(p + G * D + h);
+        ls[k] = load_partial(p + G * D + G + h);
+        x01[k] = load_partial2(p + 4 * c);
+        x23[k] = load_partial2(p + 4 * c + 2);
       }
-      for (; s < ns; ++s) o += load_partial(base + s * pf) * __builtin_amdgcn_exp2f(ml[s * 2 * G + h] - mh);
-      acc[k] = o;
-    }
-  }
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int idx = threadIdx.x + k * NT;
-    if (idx >= G * D) break;
-    const int h = idx / D;
-    const int d = idx % D;
-    const int64_t off = (static_cast<int64_t>(g.q_row) * hq + static_cast<int64_t>(g.kvh) * G + h) * D + d;
-    store_out<OT>(out, off, acc[k] / run_l[h]);
+      for (int k = 0; k < 4; ++k) fold(ms[k], ls[k], x01[k], x23[k]);
+    }
+    for (; s < g.n_parts; ++s) {
+      const float* p = base + static_cast<int64_t>(s) * pf;
+      fold(load_partial(p + G * D + h), load_partial(p + G * D + G + h), load_partial2(p + 4 * c),
+           load_partial2(p + 4 * c + 2));
+    }
+    const float inv = 1.f / l;
+    const int64_t off = (static_cast<int64_t>(g.q_row) * hq + static_cast<int64_t>(g.kvh) * G) * D + 4 * c;
+    store_out<OT>(out, off + 0, o0 * inv);
+    store_out<OT>(out, off + 1, o1 * inv);
+    store_out<OT>(out, off + 2, o2 * inv);
+    store_out<OT>(out, off + 3, o3 * inv);
   }
 }
 
@@ -341,12 +318,12 @@ __device__ __forceinline__ void merge_group(const MergeGroup& g, const float* pa
 // workgroup that finishes a group's last span merges the group's rows
 // (merge groups `group` .. `group + n_rows - 1`, which share their spans) and
 // returns the counter to zero, so the plan image can be launched again.
-// `lds` needs merge_lds_floats(G) + 1 floats and must be free when this is called.
+// `lds` needs one int and must be free when this is called.
 template <int D, int G, int OT, int NT>
 __device__ __forceinline__ void finish_split(const AttnArgs& a, int group, int n_rows, float* lds) {
   __builtin_amdgcn_s_waitcnt(0);   // this thread's partial stores have completed
   __syncthreads();
-  int* flag = reinterpret_cast<int*>(lds + merge_lds_floats(G));
+  int* flag = reinterpret_cast<int*>(lds);
   if (threadIdx.x == 0) {
     const int done = __hip_atomic_fetch_add(a.counters + group, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const bool last = done == a.groups[group].n_parts - 1;
@@ -355,7 +332,7 @@ __device__ __forceinline__ void finish_split(const AttnArgs& a, int group, int n
   }
   __syncthreads();
   if (!*flag) return;
-  for (int r = 0; r < n_rows; ++r) merge_group<D, G, OT, NT>(a.groups[group + r], a.partials, a.out, a.hq, lds);
+  for (int r = 0; r < n_rows; ++r) merge_group_direct<D, G, OT, NT>(a.groups[group + r], a.partials, a.out, a.hq);
 }
 
 // ---------------------------------------------------------------------------
@@ -1348,8 +1325,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   static_assert(!TILES || NW == kThreads / 64, "tile items run on four-wave workgroups");
   constexpr int RB = row_lds_bytes<D, G, NW>();
   constexpr int TB = TILES ? TileLds<D>::BYTES : 0;
-  static_assert(RB >= (merge_lds_floats(G) + 1) * 4 && (!TILES || TB >= (merge_lds_floats(G) + 1) * 4),
-                "a split item's workgroup merges in its own LDS");
+  static_assert(RB >= 4 && (!TILES || TB >= 4), "a split item's workgroup keeps its merge flag in LDS");
   __shared__ __align__(16) unsigned char smem[RB > TB ? RB : TB];
   const WorkItem it = a.items[blockIdx.x];
   if constexpr (TILES) {
