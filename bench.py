@@ -364,7 +364,11 @@ def budget_sweep(args, log):
     prefill-heavy batch) through planner, upload and attention on one 65,536-
     block fp8 pool of random codes and scales. Reports per budget and overall:
     query tokens per second of the attention launches (HIP events) and of
-    whole replayed steps, and the fractions of the HBM and MFMA roofs."""
+    whole replayed steps, and the fractions of the HBM and MFMA roofs. Each
+    replayed batch also runs as --sweep-layers layers back to back (each layer
+    on its own random blocks of the pool, one plan for all), timed as one
+    window: the per-layer figures of a multi-layer step, where no launch
+    waits on the host."""
     import torch
     import paper_2512_04013_amd as aug
     from paper_2512_04013_amd import runtime as rt
@@ -411,7 +415,8 @@ def budget_sweep(args, log):
         pass
 
     results = {}
-    t_all, q_all, bytes_all, flops_all, wall_all = 0.0, 0, 0.0, 0.0, 0.0
+    t_all, q_all, bytes_all, flops_all, wall_all, t_all_l = 0.0, 0, 0.0, 0.0, 0.0, 0.0
+    n_layers = max(1, int(args.sweep_layers))
     # every budget's batches are replayed twice; only the second pass is timed, so
     # no budget pays for first launches (code loading, clocks ramping up)
     for budget, (run, pick), timed_pass in [(b, rp, p) for p in (False, True) for b, rp in runs.items()]:
@@ -430,7 +435,9 @@ def budget_sweep(args, log):
             bt_start[1:] = np.cumsum(nblk)
             # a random window of one fixed random permutation of the pool
             # (distinct blocks, O(batch) host work per step)
-            bids = np.take(pool_perm, rng.integers(nb) + np.arange(int(bt_start[-1])), mode="wrap")
+            n_bt = int(bt_start[-1])
+            bids = np.concatenate([np.take(pool_perm, rng.integers(nb) + np.arange(n_bt), mode="wrap")
+                                   for _ in range(n_layers)])
             info, plan = aug.aug_attn_plan(shape, q_start, ctx, bt_start, nb, None)
             slot = k & 1
             if host_ev[slot] is not None:
@@ -441,15 +448,19 @@ def budget_sweep(args, log):
             hb.numpy()[off:off + bids.nbytes] = bids.view(np.uint8)
             aug.aug_plan_upload(hb, up_dev, off + bids.nbytes, stream=stream.cuda_stream)
             plan_dev = up_dev[:plan.size]
-            bid_dev = up_dev[off:off + bids.nbytes].view(torch.int32)
+            bid_all = up_dev[off:off + bids.nbytes].view(torch.int32)
             host_ev[slot] = torch.cuda.Event()
             host_ev[slot].record(stream)
-            e0, e1 = TimingEvent(), TimingEvent()
+            e0, e1, e2 = TimingEvent(), TimingEvent(), TimingEvent()
             e0.record(stream)
-            aug.aug_attn_mixed(shape, info, plan_dev, q, k_cache, v_cache, k_scale, v_scale, bid_dev, nb, out,
-                               ws_dev, stream=stream.cuda_stream)
-            e1.record(stream)
-            evs.append((e0, e1))
+            for layer in range(n_layers):
+                aug.aug_attn_mixed(shape, info, plan_dev, q, k_cache, v_cache, k_scale, v_scale,
+                                   bid_all[layer * n_bt:(layer + 1) * n_bt], nb, out, ws_dev,
+                                   stream=stream.cuda_stream)
+                if layer == 0:
+                    e1.record(stream)
+            e2.record(stream)
+            evs.append((e0, e1, e2))
             b = B()
             b.q_len, b.ctx_len, b.total_q = q_len, ctx, int(q_start[-1])
             b.num_kv_heads, b.num_q_heads, b.head_dim = hkv, hq, d
@@ -463,16 +474,23 @@ def budget_sweep(args, log):
         wall = time.perf_counter() - w0
         if not timed_pass:
             continue
-        times = [a.elapsed_time(c) * 1e-3 for a, c in evs]
+        times = [a.elapsed_time(c) * 1e-3 for a, c, _ in evs]
         t = sum(times)
-        by_kind = {}
-        for label, pre in (("prefill_dominated", True), ("decode_dominated", False)):
-            sel = [(tt, bb, ff) for tt, (p_dom, bb, ff) in zip(times, kinds) if p_dom == pre]
-            if sel:
-                ts = sum(x[0] for x in sel)
-                by_kind[label] = {"batches": len(sel), "attn_us_per_batch": round(1e6 * ts / len(sel), 1),
-                                  "mfma_frac": round(sum(x[2] for x in sel) / ts / (MFMA_BF16_PEAK_TFS * 1e12), 4),
-                                  "hbm_frac": round(sum(x[1] for x in sel) / ts / (HBM_PEAK_GBS * 1e9), 4)}
+        # per layer of an n_layers-layer step: the window over all layers / n_layers
+        times_l = [a.elapsed_time(e) * 1e-3 / n_layers for a, _, e in evs]
+        t_l = sum(times_l)
+
+        def by_bound(ts_all):
+            out_k = {}
+            for label, pre in (("prefill_dominated", True), ("decode_dominated", False)):
+                sel = [(tt, bb, ff) for tt, (p_dom, bb, ff) in zip(ts_all, kinds) if p_dom == pre]
+                if sel:
+                    ts = sum(x[0] for x in sel)
+                    out_k[label] = {"batches": len(sel), "attn_us_per_batch": round(1e6 * ts / len(sel), 1),
+                                    "mfma_frac": round(sum(x[2] for x in sel) / ts / (MFMA_BF16_PEAK_TFS * 1e12), 4),
+                                    "hbm_frac": round(sum(x[1] for x in sel) / ts / (HBM_PEAK_GBS * 1e9), 4)}
+            return out_k
+        by_kind = by_bound(times)
         results[budget] = {"batches_formed": len(run.steps), "trace_complete": bool(run.complete),
                            "by_bound": by_kind,
                            "batches_replayed": len(pick), "query_tokens": int(qsum),
@@ -480,11 +498,16 @@ def budget_sweep(args, log):
                            "hbm_frac": round(nbytes / t / (HBM_PEAK_GBS * 1e9), 4),
                            "mfma_frac": round(nflops / t / (MFMA_BF16_PEAK_TFS * 1e12), 4),
                            "attn_ms_per_batch": round(1e3 * t / len(pick), 4),
+                           "per_layer": {"layers": n_layers, "attn_ms_per_batch": round(1e3 * t_l / len(pick), 4),
+                                         "hbm_frac": round(nbytes / t_l / (HBM_PEAK_GBS * 1e9), 4),
+                                         "mfma_frac": round(nflops / t_l / (MFMA_BF16_PEAK_TFS * 1e12), 4),
+                                         "by_bound": by_bound(times_l)},
                            # the library former's own time per iteration over the whole trace
                            # (the paper's per-iteration scheduling overhead, Table 3)
                            "former_per_iteration": run.former_stats}
         log(f"budget {budget}: {results[budget]}")
         t_all += t
+        t_all_l += t_l
         wall_all += wall
         q_all += qsum
         bytes_all += nbytes
@@ -498,7 +521,12 @@ def budget_sweep(args, log):
         roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": None}
     roof.update({"kernel": "aug_attn_mixed launches over all replayed batches",
-                 "prefill_mfma_tflops": round(achieved_tfs, 2), "hbm_gbs": round(achieved_gbs, 1)})
+                 "prefill_mfma_tflops": round(achieved_tfs, 2), "hbm_gbs": round(achieved_gbs, 1),
+                 "per_layer": {"layers": n_layers, "hbm_gbs": round(bytes_all / t_all_l / 1e9, 1),
+                               "hbm_frac": round(bytes_all / t_all_l / 1e9 / HBM_PEAK_GBS, 4),
+                               "prefill_mfma_tflops": round(flops_all / t_all_l / 1e12, 2),
+                               "what": "each batch's attention as layers back to back, one window over all "
+                                       "layers divided by their number"}})
     n_rep = sum(len(p) for _, p in runs.values())
     result = {
         "metric": "mixed-batch attn query-tokens/s + % peak HBM GB/s (decode) / % MFMA (prefill)",
@@ -731,6 +759,8 @@ def main():
     ap.add_argument("--no-park-resume", action="store_true",
                     help="skip the separate park/resume timing of workloads that move paused requests")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--sweep-layers", type=int, default=8,
+                    help="budget sweep: layers per replayed batch for the per-layer figures")
     ap.add_argument("--sweep-batches", type=int, default=200,
                     help="budget-sweep-fp8: formed batches replayed per budget")
     ap.add_argument("--layers", type=int, default=8,
