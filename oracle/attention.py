@@ -72,12 +72,13 @@ def round_query_rows_e4m3(q_rows: np.ndarray) -> np.ndarray:
     even) and multiplied back by the scale. The scale and its reciprocal are
     float32 values (reciprocal = 448 / largest magnitude, correctly rounded;
     scale = largest magnitude times float32(1/448)), and the division is a
-    float32 product with the reciprocal, as the kernel computes them; an
-    all-zero vector stays zero. q_rows [n, H, D] float64 (bf16 values)."""
+    float32 product with the reciprocal, as the kernel computes them; a
+    vector whose largest magnitude is below 2^-100 (all zero, in practice)
+    becomes zero. q_rows [n, H, D] float64 (bf16 values)."""
     q32 = np.asarray(q_rows, dtype=np.float32)
     amax = np.abs(q32).max(axis=-1, keepdims=True)
-    zero = amax == 0
-    inv = np.where(zero, np.float32(1.0), np.float32(448.0) / np.where(zero, np.float32(1.0), amax))
+    zero = ~(amax >= np.float32(2.0 ** -100))
+    inv = np.where(zero, np.float32(0.0), np.float32(448.0) / np.where(zero, np.float32(1.0), amax))
     scale = np.where(zero, np.float32(1.0), amax * np.float32(1.0 / 448.0)).astype(np.float32)
     x = (q32 * inv.astype(np.float32)).astype(np.float32)
     codes = e4m3fn_encode(x)

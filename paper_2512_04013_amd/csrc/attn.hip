@@ -969,8 +969,11 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
             amax = fmaxf(amax, fmaxf(fabsf(__uint_as_float(w[e] << 16)), fabsf(__uint_as_float(w[e] & 0xFFFF0000u))));
         }
       amax = max_across_halves(amax);
-      qscale = amax > 0.f ? amax * (1.f / 448.f) : 1.f;
-      const float inv = amax > 0.f ? 448.f / amax : 1.f;
+      // a vector below 2^-100 (all zero, in practice) rounds to zero: its
+      // reciprocal scale would overflow
+      const bool tiny = !(amax >= 0x1p-100f);
+      qscale = tiny ? 1.f : amax * (1.f / 448.f);
+      const float inv = tiny ? 0.f : 448.f / amax;
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll

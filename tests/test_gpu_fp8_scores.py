@@ -101,3 +101,21 @@ def test_fp8_scores_are_opt_in_and_refused_elsewhere():
     info, _ = aug.aug_attn_plan(aug.make_shape(16, 2, 128, "bf16", "fp8", "bf16", 0.088), b.q_start,
                                 b.ctx_len, b.bt_start, b.num_pool_blocks)
     assert info.tile_path == aug.AUG_TILES_BF16
+
+
+def test_fp8_scores_zero_and_tiny_query_vectors():
+    """Query vectors that are all zero, or whose largest magnitude is below
+    2^-100, round to zero: their rows attend uniformly (the oracle of the
+    rounded queries says the same), with no overflow of the reciprocal scale."""
+    b = make_batch_from_lengths("fp8qz", [40, 1], [300, 90], num_q_heads=16, num_kv_heads=2, head_dim=128,
+                                q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16", n_pool_blocks=128, seed=21)
+    q = b.q.copy()                       # bf16 bit patterns [rows][heads][dim]
+    q[3, 0, :] = 0
+    q[5, 9, :] = 0
+    q[7, 4, :] = 0
+    q[7, 4, 11] = 0x0380                 # 2^-120
+    b.q = q
+    got, _ = _run(b)
+    want = oa.attention_for(b, fp8_chunk_queries=True)
+    compare(got, want, "bf16", what="zero and tiny query vectors vs rounded-Q oracle")
+    assert np.isfinite(got).all()

@@ -317,6 +317,9 @@ def test_rounded_queries_are_the_nearest_scaled_e4m3_values():
 
 def test_rounded_queries_zero_vector_and_chunk_rows_only():
     assert (oa.round_query_rows_e4m3(np.zeros((1, 1, 16))) == 0).all()
+    tiny = np.zeros((1, 1, 16))
+    tiny[0, 0, 3] = 2.0 ** -120          # its reciprocal scale would overflow float32
+    assert (oa.round_query_rows_e4m3(tiny) == 0).all()
     b = make_batch_from_lengths("fp8q", [1, 5, 1], [40, 70, 33], num_q_heads=8, num_kv_heads=2,
                                 head_dim=128, q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16",
                                 n_pool_blocks=64, seed=5)
