@@ -78,6 +78,16 @@ __device__ __forceinline__ uint32_t fp8_code(float y) {
   return code | sign;
 }
 
+// An append item read with one 16-byte load (the index is the same for the
+// whole wave, so it goes through the scalar cache).
+__device__ __forceinline__ AppendItem load_item(const AppendItem* items, int64_t idx) {
+  static_assert(sizeof(AppendItem) == 16, "one 16-byte load");
+  const uint4 raw = *reinterpret_cast<const uint4*>(items + idx);
+  AppendItem it;
+  __builtin_memcpy(&it, &raw, sizeof(it));
+  return it;
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
@@ -87,9 +97,9 @@ __global__ __launch_bounds__(kThreads) void append_copy_kernel(AppendArgs a) {
   constexpr int LPR = D * EB / 16;     // lanes per row (16 bytes each)
   constexpr int RPP = 64 / LPR;        // rows per pass
   const int lane = threadIdx.x & 63;
-  const int64_t unit = static_cast<int64_t>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
+  const int64_t unit = static_cast<int64_t>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (unit >= static_cast<int64_t>(a.num_items) * a.hkv * 2) return;
-  const AppendItem it = a.items[unit / (2 * a.hkv)];
+  const AppendItem it = load_item(a.items, unit / (2 * a.hkv));
   const int kvh = static_cast<int>((unit >> 1) % a.hkv);
   const bool is_v = unit & 1;
   const int32_t bid = a.block_ids[it.bt_index];
@@ -112,13 +122,15 @@ __global__ __launch_bounds__(kThreads) void append_fp8_kernel(AppendArgs a) {
   constexpr int RPP = 64 / LPR;        // 4 rows per pass
   constexpr int PASSES = kBlock / RPP;
   const int lane = threadIdx.x & 63;
-  const int64_t unit = static_cast<int64_t>(blockIdx.x) * kWaves + (threadIdx.x >> 6);
+  const int64_t unit = static_cast<int64_t>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (unit >= static_cast<int64_t>(a.num_items) * a.hkv * 2) return;
-  const AppendItem it = a.items[unit / (2 * a.hkv)];
+  const AppendItem it = load_item(a.items, unit / (2 * a.hkv));
   const int kvh = static_cast<int>((unit >> 1) % a.hkv);
   const bool is_v = unit & 1;
+  // the block id and the new rows are fetched together, the block's current
+  // scale as soon as the id is known: no load waits on another it does not need
   const int32_t bid = a.block_ids[it.bt_index];
-  if (static_cast<uint32_t>(bid) >= static_cast<uint32_t>(a.num_pool_blocks)) return;
+  const bool bid_ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
   const uint16_t* src = reinterpret_cast<const uint16_t*>(is_v ? a.v_new : a.k_new);
   uint8_t* blk = reinterpret_cast<uint8_t*>(is_v ? a.v_cache : a.k_cache) +
                  (static_cast<int64_t>(bid) * a.hkv + kvh) * kBlock * D;
@@ -141,13 +153,14 @@ __global__ __launch_bounds__(kThreads) void append_fp8_kernel(AppendArgs a) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf(x[p][e]));
   }
+  const float s_old = bid_ok && it.slot0 > 0 ? *scale : 0.f;
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, 64));
+  if (!bid_ok) return;
 
   const float need = amax / 448.f;
   float s = need;
   if (it.slot0 > 0) {
-    const float s_old = *scale;
     if (need > s_old) {
       // the scale grows: re-encode the block's earlier tokens
       for (int r = r0; r < it.slot0; r += RPP) {
