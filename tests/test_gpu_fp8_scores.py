@@ -119,3 +119,21 @@ def test_fp8_scores_zero_and_tiny_query_vectors():
     want = oa.attention_for(b, fp8_chunk_queries=True)
     compare(got, want, "bf16", what="zero and tiny query vectors vs rounded-Q oracle")
     assert np.isfinite(got).all()
+
+
+def test_fp8_scores_relaunch_repeats_the_bits():
+    """Split tiles and split decode rows on the fp8 score path: the same plan
+    image launched three times gives the same bits (the counters it uses are
+    back at zero after each launch)."""
+    q_lens, ctx_lens, hq, hkv = CASES[1]
+    b = make_batch_from_lengths("fp8qk-relaunch", q_lens, ctx_lens, num_q_heads=hq, num_kv_heads=hkv,
+                                head_dim=128, q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16",
+                                n_pool_blocks=1024, seed=77)
+    first, att = _run(b, kv_split=48)
+    assert att.info.num_merge_groups > 0 and att.info.num_prefill_items > 0
+    from paper_2512_04013_amd import runtime as rt
+    for _ in range(2):
+        shape, kv, q, bids = rt.upload_batch(b, staging_bytes=1 << 26)
+        out = att.run(q, kv=kv, block_ids=bids)
+        torch.cuda.synchronize()
+        assert np.array_equal(rt.to_host_f64(out), first)
