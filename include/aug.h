@@ -157,8 +157,9 @@ typedef enum { AUG_ROWS_AUTO = 0, AUG_ROWS_VALU = 1, AUG_ROWS_MFMA = 2 } aug_row
 /* Arithmetic of the prefill tiles' score products S = Q K^T. BF16: Q and
  * the (converted) keys as bf16 on 32x32x16 MFMAs, the default. FP8_QK, for
  * fp8 KV with bf16 Q and head_dim 128 only: the keys stay fp8 and each query
- * row is rounded to E4M3 with its own scale (largest magnitude / 448), on
- * 32x32x64 fp8 MFMAs at twice the rate; P V stays bf16. Rounding Q to 3
+ * vector (row and head) is rounded to E4M3 with its own scale (largest
+ * magnitude / 448; a vector below 2^-100 becomes zero), on 32x32x64 fp8
+ * MFMAs at twice the rate; P V stays bf16; decode rows are not affected. Rounding Q to 3
  * mantissa bits moves a logit by about 2^-5 of |q| |k| sqrt(head_dim) times
  * the softmax scale, so outputs stay within the bf16 tolerances for
  * near-uniform attention (keys of norm about 1) but not for sharp attention
