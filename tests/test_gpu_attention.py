@@ -292,3 +292,19 @@ def test_decodes_at_very_long_contexts(kv):
     got, att = _run(b)
     assert att.info.num_merge_groups >= 2
     compare(got, oa.attention_for(b), "bf16", what=f"long decodes {kv} items={att.info.num_items}")
+
+
+@pytest.mark.parametrize("hq,kv", [(32, "bf16"), (64, "fp8"), (64, "bf16")])
+def test_decode_rows_with_a_thousand_spans(hq, kv):
+    """Decode rows split into about 1250 spans each (16-key spans over 20,000
+    keys), merged inside the launch by the workgroup that finishes last:
+    the merge loop over many partials, on the vector-ALU rows (four heads per
+    KV head) and on the eight-wave MFMA rows (eight heads, fp8 and bf16)."""
+    ctx_lens = [20000, 19999, 700, 1]
+    b = make_batch_from_lengths("many-spans", [1, 1, 1, 1], ctx_lens, num_q_heads=hq, num_kv_heads=8,
+                                head_dim=128, q_dtype="bf16", kv_dtype=kv, out_dtype="bf16",
+                                n_pool_blocks=int(sum(-(-c // 16) for c in ctx_lens)) + 8, seed=79, kv_std=1.0)
+    say(f"[many spans] G={hq // 8} kv={kv}")
+    got, att = _run(b, kv_split=16)
+    assert att.info.num_partials >= 2 * 8 * 1250
+    compare(got, oa.attention_for(b), "bf16", what=f"many spans G={hq // 8} {kv} parts={att.info.num_partials}")
