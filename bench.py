@@ -64,11 +64,13 @@ WORKLOADS = {
 }
 # timed after the main (mixed-batch) workload in the default run, each with its own roofline
 # (a workload name followed by "@valu" runs its row items on the vector ALUs instead of the
-# planner's default, which is MFMA for eight query heads per KV head; "@fp8qk" runs the
+# planner's default, which is MFMA for eight query heads per KV head; "@mfma" runs four-head
+# groups' row items on the MFMA row path, which they take only when asked; "@fp8qk" runs the
 # prefill tiles' score products on fp8 MFMAs, an opt-in arithmetic)
-DEFAULT_ALSO = ("decode-8b", "long-context-8b", "prefill-fp8-64x8", "prefill-fp8-64x8@fp8qk", "decode-fp8-64x8",
-                "decode-fp8-64x8@valu")
-PATHS = {"": (0, 0), "valu": (1, 0), "fp8qk": (0, 2)}   # suffix -> (row path, tile path)
+DEFAULT_ALSO = ("mixed-8b@mfma", "decode-8b", "decode-8b@mfma", "long-context-8b", "prefill-fp8-64x8",
+                "prefill-fp8-64x8@fp8qk", "decode-fp8-64x8", "decode-fp8-64x8@valu")
+PATHS = {"": (0, 0), "valu": (1, 0), "mfma": (2, 0), "fp8qk": (0, 2)}   # suffix -> (row path, tile path)
+PATH_NOTES = {"": "", "valu": " (vector-ALU rows)", "mfma": " (MFMA rows)", "fp8qk": " (fp8 scores)"}
 
 
 def algorithmic_bytes(b) -> float:
@@ -748,9 +750,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--tile-path", choices=("auto", "fp8qk"), default="auto",
                     help="fp8qk: the prefill tiles' score products on fp8 MFMAs (opt-in arithmetic)")
-    ap.add_argument("--row-path", choices=("auto", "valu"), default="auto",
+    ap.add_argument("--row-path", choices=("auto", "valu", "mfma"), default="auto",
                     help="where the main workload's row items run: the planner's choice (MFMA for eight query "
-                         "heads per KV head) or the vector ALUs")
+                         "heads per KV head), the vector ALUs, or MFMA (eight or four heads per KV head)")
     ap.add_argument("--kv-split", type=int, default=0, help="keys per decode work item (0: planner's choice)")
     ap.add_argument("--pool-copies", type=int, default=0,
                     help="copies of the KV pool used in turn (0: enough for 1 GiB of KV reads between "
@@ -786,7 +788,8 @@ def main():
     if args.workload == "budget-sweep-fp8":
         budget_sweep(args, log)
         return
-    result = run_workload(args.workload, args, log, full=True, row_path=1 if args.row_path == "valu" else 0,
+    result = run_workload(args.workload, args, log, full=True,
+                          row_path={"auto": 0, "valu": 1, "mfma": 2}[args.row_path],
                           tile_path=2 if args.tile_path == "fp8qk" else 0)
     if args.also is None:
         also = list(DEFAULT_ALSO) if args.workload == "mixed-8b" else []
@@ -802,7 +805,7 @@ def main():
         torch.cuda.empty_cache()
         sub = run_workload(name, args, log, full=False, row_path=PATHS[path][0], tile_path=PATHS[path][1])
         keep = ("value", "unit", "steps", "warmup", "ms_per_step", "dtype", "config", "roofline", "kv_append")
-        key = sub["config"]["workload"] + {"": "", "valu": " (vector-ALU rows)", "fp8qk": " (fp8 scores)"}[path]
+        key = sub["config"]["workload"] + PATH_NOTES[path]
         result["workloads"][key] = {k: sub[k] for k in keep}
         log(f"{name}: {sub['value']:.0f} query-tokens/s, {sub['roofline']['unit']} frac "
             f"{sub['roofline']['frac']}")

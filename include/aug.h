@@ -147,11 +147,12 @@ typedef struct {
   int32_t tile_path;         /* aug_tile_path the plan's prefill tiles run on (resolved) */
 } aug_attn_plan_info;
 
-/* Where the row items (decode rows) of a plan run. Groups of eight query
- * heads per KV head with head_dim 128 and bf16 or fp8 KV can run their
- * products on 16x16 bf16 MFMAs (the vector ALUs cannot keep up with eight
- * heads of fp8 KV); every other shape runs on the vector ALUs. AUTO takes
- * MFMA where it can, VALU otherwise. */
+/* Where the row items (decode rows) of a plan run. Groups of eight or four
+ * query heads per KV head with head_dim 128 and bf16 or fp8 KV can run their
+ * products on 16x16 bf16 MFMAs; every other shape runs on the vector ALUs.
+ * AUTO takes MFMA for groups of eight (the vector ALUs cannot keep up with
+ * eight heads of fp8 KV) and VALU otherwise; four-head groups run on MFMA
+ * only when asked for. */
 typedef enum { AUG_ROWS_AUTO = 0, AUG_ROWS_VALU = 1, AUG_ROWS_MFMA = 2 } aug_row_path;
 
 /* Arithmetic of the prefill tiles' score products S = Q K^T. BF16: Q and

@@ -14,9 +14,10 @@
 //    running (max, sum, output) state; the states are merged across lane
 //    groups with cross-lane shuffles and across waves through LDS. Each KV byte
 //    is read once for all G heads (grouped-query sharing). Arithmetic runs on
-//    the vector ALUs in fp32, except for groups of eight query heads (bf16 or
-//    fp8 KV, head_dim 128), whose products run on 16x16 bf16 MFMAs with the
-//    same item, split and merge structure (row_item_mfma).
+//    the vector ALUs in fp32, except for groups of eight (or, when asked for,
+//    four) query heads (bf16 or fp8 KV, head_dim 128), whose products run on
+//    16x16 bf16 MFMAs with the same item, split and merge structure
+//    (row_item_mfma).
 //  * Tile items (bf16 chunked prefill): 128 query rows (positions x group
 //    heads) of one chunk, causal against keys 0 .. last row's position. K and V
 //    are staged through LDS 64 keys at a time (V read back through transposing
@@ -576,14 +577,16 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
 }
 
 // ---------------------------------------------------------------------------
-// row items of 8-way grouped-query attention (MFMA)
+// row items of 8-way (and 4-way) grouped-query attention (MFMA)
 // ---------------------------------------------------------------------------
 //
 // With eight query heads per KV head, a decode row's work per KV byte (two
 // bf16 dot products of D per head and key) is more than the vector ALUs keep
 // up with next to fp8 decoding, so the eight heads go through 16x16 bf16
-// MFMAs instead (heads 8..15 of each MFMA are zero padding). Per 16-token
-// block and wave:
+// MFMAs instead (heads 8..15 of each MFMA are zero padding). Groups of four
+// heads take the same path with heads 4..15 as padding: the vector ALUs keep
+// up there, and the MFMA form only frees issue slots for the loads. Per
+// 16-token block and wave:
 //   S^T[16 keys][16 heads] = K Q^T with four 16x16x32 MFMAs over head_dim.
 //     Lane l holds token l % 16 and dims 32g .. 32g + 31 (g = l / 16) of the
 //     block's K rows; k-step s takes dims 32g + 8s .. + 8 of both K and Q (a
@@ -686,9 +689,10 @@ template <> struct MfmaRowKv<KV_FP8> {
   }
 };
 
-template <int KVT, int OT, int NW>
+template <int KVT, int OT, int NW, int G>
 __device__ void row_item_mfma(const WorkItem& it, const AttnArgs& a, float* lds) {
-  constexpr int D = 128, G = 8;
+  static_assert(G == 8 || G == 4, "one 16-column MFMA holds the group's heads");
+  constexpr int D = 128;
   constexpr bool FP8 = KVT == KV_FP8;
   using KV = MfmaRowKv<KVT>;
   constexpr int EB = KV::EB;
@@ -696,7 +700,7 @@ __device__ void row_item_mfma(const WorkItem& it, const AttnArgs& a, float* lds)
   // wave-uniform, so block ids and scales come through scalar loads instead
   // of queueing behind the K/V loads
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int j = lane & 15;            // query head of the group (8..15: padding)
+  const int j = lane & 15;            // query head of the group (G..15: padding)
   const int g = lane >> 4;            // keys 4g .. 4g + 3 of a block
   const int kvh = it.kvh;
 
@@ -704,7 +708,7 @@ __device__ void row_item_mfma(const WorkItem& it, const AttnArgs& a, float* lds)
   uint4 qop[4];
   {
     const uint16_t* qb = static_cast<const uint16_t*>(a.q) +
-                         (static_cast<int64_t>(it.q_row0) * a.hq + static_cast<int64_t>(kvh) * G + (j & 7)) * D + 32 * g;
+                         (static_cast<int64_t>(it.q_row0) * a.hq + static_cast<int64_t>(kvh) * G + (j < G ? j : 0)) * D + 32 * g;
 #pragma unroll
     for (int s = 0; s < 4; ++s) qop[s] = j < G ? *reinterpret_cast<const uint4*>(qb + 8 * s) : uint4{0, 0, 0, 0};
   }
@@ -1317,10 +1321,10 @@ template <int D, int G, int NW>
 constexpr int row_lds_bytes() { return NW * G * (D + 2) * 4; }
 
 // Whether row items of this instantiation can run on the 16x16 MFMA row
-// path (eight query heads per KV head, head_dim 128, bf16 or fp8 KV).
+// path (eight or four query heads per KV head, head_dim 128, bf16 or fp8 KV).
 template <int KVT, int D, int G, int QT>
 constexpr bool row_mfma_capable() {
-  return G == 8 && D == 128 && (KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16;
+  return (G == 8 || G == 4) && D == 128 && (KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16;
 }
 
 template <int KVT, int D, int G, int QT, int OT, bool TILES, bool ROW_MFMA, int NW, bool QK8 = false>
@@ -1340,7 +1344,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   // row items always fetch a wave's next block while the current one is
   // computed: short spans (small batches) are latency bound otherwise
   if constexpr (ROW_MFMA && row_mfma_capable<KVT, D, G, QT>())
-    row_item_mfma<KVT, OT, NW>(it, a, reinterpret_cast<float*>(smem));
+    row_item_mfma<KVT, OT, NW, G>(it, a, reinterpret_cast<float*>(smem));
   else
     row_item<KVT, D, G, QT, OT, true, NW>(it, a, reinterpret_cast<float*>(smem));
 }

@@ -33,7 +33,7 @@ bool dtype_set_supported(const aug_attn_shape& s) {
 }
 
 bool row_mfma_supported(const aug_attn_shape& s) {
-  return s.num_q_heads == 8 * s.num_kv_heads && s.head_dim == 128 && s.q_dtype == AUG_BF16 &&
+  return (s.num_q_heads == 8 * s.num_kv_heads || s.num_q_heads == 4 * s.num_kv_heads) && s.head_dim == 128 && s.q_dtype == AUG_BF16 &&
          (s.kv_dtype == AUG_BF16 || s.kv_dtype == AUG_FP8_E4M3FN);
 }
 
@@ -164,9 +164,13 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
   if (row_path != AUG_ROWS_AUTO && row_path != AUG_ROWS_VALU && row_path != AUG_ROWS_MFMA)
     return fail(AUG_ERR_INVALID, "%s: unknown row path %d", who, row_path);
   if (row_path == AUG_ROWS_MFMA && !row_mfma_supported(*s))
-    return fail(AUG_ERR_UNSUPPORTED, "%s: the MFMA row path needs 8 query heads per KV head, head_dim 128 and "
-                "bf16 or fp8 KV", who);
-  if (row_path == AUG_ROWS_AUTO) row_path = row_mfma_supported(*s) ? AUG_ROWS_MFMA : AUG_ROWS_VALU;
+    return fail(AUG_ERR_UNSUPPORTED, "%s: the MFMA row path needs 8 or 4 query heads per KV head, head_dim 128 "
+                "and bf16 or fp8 KV", who);
+  // AUTO takes the MFMA rows only for eight-head groups, where the vector ALUs
+  // cannot keep up with the KV stream; four-head groups stay on the vector ALUs
+  // unless asked for
+  if (row_path == AUG_ROWS_AUTO)
+    row_path = row_mfma_supported(*s) && s->num_q_heads == 8 * s->num_kv_heads ? AUG_ROWS_MFMA : AUG_ROWS_VALU;
   int32_t tile_path = opts->tile_path;
   if (tile_path != AUG_TILES_AUTO && tile_path != AUG_TILES_BF16 && tile_path != AUG_TILES_FP8_QK)
     return fail(AUG_ERR_INVALID, "%s: unknown tile path %d", who, tile_path);

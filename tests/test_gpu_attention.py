@@ -57,6 +57,12 @@ CASES = [
 ]
 
 
+def _row_paths(hq, hkv, d, dt):
+    """The automatic row path, and for four-head groups (head_dim 128, bf16
+    queries) also the opt-in MFMA row path."""
+    return (0, 2) if hq == 4 * hkv and d == 128 and dt in ("bf16", "fp8") else (0,)
+
+
 @pytest.mark.parametrize("case", range(len(CASES)))
 @pytest.mark.parametrize("sharp", [False, True])
 def test_ragged_shapes(case, sharp):
@@ -67,10 +73,13 @@ def test_ragged_shapes(case, sharp):
                                 n_pool_blocks=512, seed=100 + case,
                                 kv_std=1.0 if sharp else 1.0 / np.sqrt(d))
     say(f"[ragged] case={case} sharp={sharp} G={hq // hkv} D={d} kv={dt}")
-    for split in (0, 48):
-        got, att = _run(b, kv_split=split)
-        want = oa.attention_for(b)
-        compare(got, want, qd, what=f"case{case} sharp={sharp} split={split} tiles={att.info.num_prefill_items}")
+    want = oa.attention_for(b)
+    for row_path in _row_paths(hq, hkv, d, dt):
+        for split in (0, 48):
+            got, att = _run(b, kv_split=split, row_path=row_path)
+            assert row_path == 0 or att.info.row_path == row_path
+            compare(got, want, qd, what=f"case{case} sharp={sharp} split={split} row path {att.info.row_path} "
+                                        f"tiles={att.info.num_prefill_items}")
 
 
 def test_relaunching_one_plan_image_repeats_the_bits():
@@ -106,13 +115,22 @@ def decode_8b():
     return synth.make_decode_8b(seed=0)
 
 
+@pytest.fixture(scope="module")
+def decode_8b_want(decode_8b):
+    return oa.attention_for(decode_8b)
+
+
 @pytest.mark.parametrize("split", [0, 128, 1024])
-def test_decode_8b_full(decode_8b, split):
+@pytest.mark.parametrize("row_path", [0, 2])
+def test_decode_8b_full(decode_8b, decode_8b_want, split, row_path):
+    """All 256 rows of the 8B decode batch (32/8 heads), on the planner's row
+    path (vector ALU) and on the opt-in MFMA row path for four-head groups."""
     b = decode_8b
-    say(f"[decode-8b] 256 decodes, split={split}")
-    got, att = _run(b, kv_split=split)
-    want = oa.attention_for(b)
-    compare(got, want, "bf16", what=f"decode-8b split={split} items={att.info.num_items}")
+    say(f"[decode-8b] 256 decodes, split={split} row_path={row_path}")
+    got, att = _run(b, kv_split=split, row_path=row_path)
+    assert att.info.row_path == (row_path or 1)
+    compare(got, decode_8b_want, "bf16", what=f"decode-8b split={split} row path {att.info.row_path} "
+                                             f"items={att.info.num_items}")
 
 
 @pytest.mark.parametrize("kv", ["fp8", "bf16"])
@@ -139,11 +157,13 @@ def test_gqa8_decode_batch_full_size(kv, sharp, row_path):
     compare(got, oa.attention_for(b), "bf16", what=f"gqa8 decode {kv} sharp={sharp} row path {row_path} (all 512 rows)")
 
 
-def test_decode_8b_sharp_full():
+@pytest.mark.parametrize("row_path", [0, 2])
+def test_decode_8b_sharp_full(row_path):
     b = synth.make_decode_8b(seed=1, sharp=True)
-    say("[decode-8b sharp] 256 decodes")
-    got, _ = _run(b)
-    compare(got, oa.attention_for(b), "bf16", what="decode-8b sharp")
+    say(f"[decode-8b sharp] 256 decodes row_path={row_path}")
+    got, att = _run(b, row_path=row_path)
+    assert att.info.row_path == (row_path or 1)
+    compare(got, oa.attention_for(b), "bf16", what=f"decode-8b sharp row path {att.info.row_path}")
 
 
 def test_block_permutation_gives_identical_bits(decode_8b):
@@ -171,7 +191,7 @@ def test_results_do_not_depend_on_the_split_beyond_tolerance(decode_8b):
 
 # ---- the mixed batch: resume parked requests, then attention ----------------------------------
 
-def _park_resume_then_attend(b, split=0, staging_bytes=1 << 26, sample=None):
+def _park_resume_then_attend(b, split=0, staging_bytes=1 << 26, sample=None, row_path=0):
     from paper_2512_04013_amd import runtime as rt
     shape, kv, q, bids = rt.upload_batch(b, staging_bytes=staging_bytes)
     pk = b.park
@@ -189,7 +209,8 @@ def _park_resume_then_attend(b, split=0, staging_bytes=1 << 26, sample=None):
     kv.v_cache.view(torch.uint8)[src.long()] = 0xFF
     kv.resume(pk.resume_blocks, dst, host)
     att = rt.MixedAttention(shape, kv, b.q_start, b.ctx_len, b.bt_start, b.block_ids, bids,
-                            kv_split_tokens=split)
+                            kv_split_tokens=split, row_path=row_path)
+    assert row_path == 0 or att.info.row_path == row_path
     out = att.run(q)
     parked_others = None
     if len(pk.park_blocks):
@@ -220,31 +241,35 @@ def test_mixed_8b_small_all_rows():
     compare(got, want, "bf16", what="mixed-8b small")
 
 
-@pytest.mark.parametrize("sharp", [False, True])
-def test_mixed_8b_full_size_every_row(sharp):
+@pytest.mark.parametrize("sharp,row_path", [(False, 0), (True, 0), (False, 2), (True, 2)])
+def test_mixed_8b_full_size_every_row(sharp, row_path):
     """The full mixed batch (3 x 512-row prefill chunks and 512 decodes, 30 %
     of them resumed after a real park round trip), in the launch configuration
     the benchmark times (planner's split): every row against the oracle, plain
-    (K/V ~ N(0,1)/sqrt(128)) and sharp (K/V ~ N(0,1))."""
+    (K/V ~ N(0,1)/sqrt(128)) and sharp (K/V ~ N(0,1)); decode rows on the
+    planner's vector-ALU rows and on the opt-in MFMA rows."""
     b = synth.make_mixed_8b(seed=0, sharp=sharp)
-    say(f"[mixed-8b full] sharp={sharp} {b.num_reqs} requests, {b.total_q} rows, "
+    say(f"[mixed-8b full] sharp={sharp} row_path={row_path} {b.num_reqs} requests, {b.total_q} rows, "
         f"resume {len(b.park.resume_blocks)} blocks")
-    got, att, (k_res, v_res) = _park_resume_then_attend(b, staging_bytes=1 << 27)
+    got, att, (k_res, v_res) = _park_resume_then_attend(b, staging_bytes=1 << 27, row_path=row_path)
     assert att.info.num_prefill_items > 0
     want = oa.attention_for(b, k_cache=k_res, v_cache=v_res)
-    compare(got, want, "bf16", what=f"mixed-8b full sharp={sharp} (all {b.total_q} rows)")
+    compare(got, want, "bf16", what=f"mixed-8b full sharp={sharp} row path {att.info.row_path} "
+                                    f"(all {b.total_q} rows)")
 
 
-@pytest.mark.parametrize("sharp", [False, True])
-def test_long_context_every_row(sharp):
+@pytest.mark.parametrize("sharp,row_path", [(False, 0), (True, 0), (True, 2)])
+def test_long_context_every_row(sharp, row_path):
     """64 decodes over 16k-32k keys (split-K, merged inside the launch) after
-    8 requests were parked and 8 resumed: all 64 rows against the oracle."""
+    8 requests were parked and 8 resumed: all 64 rows against the oracle, on
+    the planner's row path and (sharp inputs) on the opt-in MFMA rows."""
     b = synth.make_long_context(seed=0, sharp=sharp)
-    say(f"[long-context] sharp={sharp} 64 decodes 16k-32k, resume 8, park 8 ({len(b.park.park_blocks)} blocks)")
-    got, att, (k_res, v_res) = _park_resume_then_attend(b, staging_bytes=1 << 28)
+    say(f"[long-context] sharp={sharp} row_path={row_path} 64 decodes 16k-32k, resume 8, park 8 "
+        f"({len(b.park.park_blocks)} blocks)")
+    got, att, (k_res, v_res) = _park_resume_then_attend(b, staging_bytes=1 << 28, row_path=row_path)
     assert att.info.num_merge_groups > 0
     want = oa.attention_for(b, k_cache=k_res, v_cache=v_res)
-    compare(got, want, "bf16", what=f"long-context sharp={sharp} (all 64 rows)")
+    compare(got, want, "bf16", what=f"long-context sharp={sharp} row path {att.info.row_path} (all 64 rows)")
 
 
 @pytest.mark.parametrize("workload,sharp", [("prefill-fp8-64x8", False), ("prefill-fp8-64x8", True),
@@ -279,32 +304,36 @@ def test_long_chunk_over_long_prior_context():
             what=f"long chunk items={att.info.num_items} tile merges={att.info.num_tile_merge_groups}")
 
 
-@pytest.mark.parametrize("kv", ["bf16"])
-def test_decodes_at_very_long_contexts(kv):
+@pytest.mark.parametrize("kv,row_path", [("bf16", 0), ("bf16", 2), ("fp8", 2)])
+def test_decodes_at_very_long_contexts(kv, row_path):
     """Decodes over 131,072 and 131,071 keys (8192 blocks each, many split
-    spans merged inside the launch) beside a one-key decode."""
+    spans merged inside the launch) beside a one-key decode, four heads per
+    KV head: the vector-ALU rows and the opt-in MFMA rows."""
     hq = 32
     ctx_lens = [131072, 131071, 1]
     b = make_batch_from_lengths("long-decodes", [1, 1, 1], ctx_lens, num_q_heads=hq, num_kv_heads=8, head_dim=128,
                                 q_dtype="bf16", kv_dtype=kv, out_dtype="bf16",
                                 n_pool_blocks=int(sum(-(-c // 16) for c in ctx_lens)) + 8, seed=78, kv_std=1.0)
-    say(f"[long decodes] kv={kv} ctx={ctx_lens}")
-    got, att = _run(b)
-    assert att.info.num_merge_groups >= 2
-    compare(got, oa.attention_for(b), "bf16", what=f"long decodes {kv} items={att.info.num_items}")
+    say(f"[long decodes] kv={kv} row_path={row_path} ctx={ctx_lens}")
+    got, att = _run(b, row_path=row_path)
+    assert att.info.num_merge_groups >= 2 and att.info.row_path == (row_path or 1)
+    compare(got, oa.attention_for(b), "bf16", what=f"long decodes {kv} row path {att.info.row_path} "
+                                                   f"items={att.info.num_items}")
 
 
-@pytest.mark.parametrize("hq,kv", [(32, "bf16"), (64, "fp8"), (64, "bf16")])
-def test_decode_rows_with_a_thousand_spans(hq, kv):
+@pytest.mark.parametrize("hq,kv,row_path", [(32, "bf16", 0), (32, "fp8", 2), (64, "fp8", 0), (64, "bf16", 0)])
+def test_decode_rows_with_a_thousand_spans(hq, kv, row_path):
     """Decode rows split into about 1250 spans each (16-key spans over 20,000
     keys), merged inside the launch by the workgroup that finishes last:
     the merge loop over many partials, on the vector-ALU rows (four heads per
-    KV head) and on the eight-wave MFMA rows (eight heads, fp8 and bf16)."""
+    KV head) and on the eight-wave MFMA rows (eight heads, fp8 and bf16; four
+    heads when asked for)."""
     ctx_lens = [20000, 19999, 700, 1]
     b = make_batch_from_lengths("many-spans", [1, 1, 1, 1], ctx_lens, num_q_heads=hq, num_kv_heads=8,
                                 head_dim=128, q_dtype="bf16", kv_dtype=kv, out_dtype="bf16",
                                 n_pool_blocks=int(sum(-(-c // 16) for c in ctx_lens)) + 8, seed=79, kv_std=1.0)
-    say(f"[many spans] G={hq // 8} kv={kv}")
-    got, att = _run(b, kv_split=16)
+    say(f"[many spans] G={hq // 8} kv={kv} row_path={row_path}")
+    got, att = _run(b, kv_split=16, row_path=row_path)
+    assert row_path == 0 or att.info.row_path == row_path
     assert att.info.num_partials >= 2 * 8 * 1250
     compare(got, oa.attention_for(b), "bf16", what=f"many spans G={hq // 8} {kv} parts={att.info.num_partials}")

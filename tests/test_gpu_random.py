@@ -96,12 +96,16 @@ def _check_random_case(case, seed, lengths, splits):
     want = oa.attention_for(b, k_cache=k, v_cache=v, k_scale=ks, v_scale=vs)
     compare(got, want, qd, what=f"random seed {seed} items={att.info.num_items} tiles={att.info.num_prefill_items} "
                                 f"groups={att.info.num_merge_groups} row path {att.info.row_path}")
-    if att.info.row_path == 2:
-        # eight-head groups: the vector-ALU row path over the same appended cache
-        import paper_2512_04013_amd as aug
+    import paper_2512_04013_amd as aug
+    other = None
+    if att.info.row_path == aug.AUG_ROWS_MFMA:
+        other = aug.AUG_ROWS_VALU          # eight-head groups: also the vector-ALU rows
+    elif hq == 4 * hkv and d == 128 and qd == "bf16":
+        other = aug.AUG_ROWS_MFMA          # four-head groups: also the opt-in MFMA rows
+    if other is not None:
         att2 = rt.MixedAttention(shape, kvp, b.q_start, b.ctx_len, b.bt_start, b.block_ids, bids,
-                                 kv_split_tokens=split, row_path=aug.AUG_ROWS_VALU)
-        assert att2.info.row_path == aug.AUG_ROWS_VALU
+                                 kv_split_tokens=split, row_path=other)
+        assert att2.info.row_path == other
         got2 = rt.to_host_f64(att2.run(q))
         torch.cuda.synchronize()
-        compare(got2, want, qd, what=f"random seed {seed} vector-ALU row path")
+        compare(got2, want, qd, what=f"random seed {seed} row path {other}")

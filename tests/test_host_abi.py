@@ -308,8 +308,9 @@ def test_a_plan_for_one_shape_is_refused_for_another():
 def test_row_path_option_resolves_and_is_checked():
     """AUTO runs eight-head groups (head_dim 128, bf16 or fp8 KV) on the MFMA
     row path and everything else on the vector ALUs; VALU can be asked for
-    anywhere, MFMA only where it exists. The resolved path is in the info and
-    the plan header, and a call refuses an info naming a path its shape lacks."""
+    anywhere, MFMA only where it exists (groups of eight or four heads). The
+    resolved path is in the info and the plan header, and a call refuses an
+    info naming a path its shape lacks."""
     L = aug.lib()
     ctx = [700, 3000, 17]
     q_start, bt_start = [0, 1, 2, 3], np.concatenate([[0], np.cumsum([-(-c // 16) for c in ctx])])
@@ -322,9 +323,14 @@ def test_row_path_option_resolves_and_is_checked():
     assert info.row_path == aug.AUG_ROWS_VALU and plan[61] == aug.AUG_ROWS_VALU
     info4, _ = aug.aug_attn_plan(g4, q_start, ctx, bt_start, pool)
     assert info4.row_path == aug.AUG_ROWS_VALU
-    with pytest.raises(AugError) as e:
-        aug.aug_attn_plan(g4, q_start, ctx, bt_start, pool, row_path=aug.AUG_ROWS_MFMA)
-    assert e.value.status == aug.AUG_ERR_UNSUPPORTED
+    info4m, plan4m = aug.aug_attn_plan(g4, q_start, ctx, bt_start, pool, row_path=aug.AUG_ROWS_MFMA)
+    assert info4m.row_path == aug.AUG_ROWS_MFMA and plan4m[61] == aug.AUG_ROWS_MFMA
+    for hq, hkv, d, kv in [(16, 8, 128, "bf16"), (64, 8, 64, "bf16"), (32, 8, 128, "f32"), (64, 4, 128, "bf16")]:
+        other = aug.make_shape(hq, hkv, d, "f32" if kv == "f32" else "bf16", kv, "f32" if kv == "f32" else "bf16",
+                               0.088)
+        with pytest.raises(AugError) as e:
+            aug.aug_attn_plan(other, q_start, ctx, bt_start, pool, row_path=aug.AUG_ROWS_MFMA)
+        assert e.value.status == aug.AUG_ERR_UNSUPPORTED, (hq, hkv, d, kv)
     with pytest.raises(AugError) as e:
         aug.aug_attn_plan(g8, q_start, ctx, bt_start, pool, row_path=7)
     assert e.value.status == aug.AUG_ERR_INVALID
@@ -334,9 +340,12 @@ def test_row_path_option_resolves_and_is_checked():
     out = aug.aug_attn_plan_info()
     assert L.aug_attn_plan_opts(aug.C.byref(g8), aug.C.byref(desc), aug.C.byref(opts), None, 0,
                                 aug.C.byref(out)) == aug.AUG_ERR_INVALID
-    bad = aug.aug_attn_plan_info.from_buffer_copy(info4)
+    g2 = aug.make_shape(16, 8, 128, "bf16", "bf16", "bf16", 0.088)
+    info2, _ = aug.aug_attn_plan(g2, q_start, ctx, bt_start, pool)
+    assert info2.row_path == aug.AUG_ROWS_VALU
+    bad = aug.aug_attn_plan_info.from_buffer_copy(info2)
     bad.row_path = aug.AUG_ROWS_MFMA
-    st = L.aug_attn_mixed(aug.C.byref(g4), aug.C.byref(bad), 8, 8, 8, 8, None, None, 8, pool, 8, 8, 1 << 40, None)
+    st = L.aug_attn_mixed(aug.C.byref(g2), aug.C.byref(bad), 8, 8, 8, 8, None, None, 8, pool, 8, 8, 1 << 40, None)
     assert st == aug.AUG_ERR_INVALID and "row path" in aug.aug_last_error()
 
 
@@ -361,6 +370,7 @@ def test_default_split_doubles_for_mfma_rows_without_tiles():
     assert plan(g8, [1] * 20, small, kv_split_tokens=300).kv_split_tokens == 304
     g4 = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)
     assert plan(g4, [1] * 20, small).kv_split_tokens == 512
+    assert plan(g4, [1] * 20, small, row_path=aug.AUG_ROWS_MFMA).kv_split_tokens == 1024
 
 
 def test_tile_path_option_resolves_and_is_checked():
