@@ -66,11 +66,12 @@ WORKLOADS = {
 # (a workload name followed by "@valu" runs its row items on the vector ALUs instead of the
 # planner's default, which is MFMA for eight query heads per KV head; "@mfma" runs four-head
 # groups' row items on the MFMA row path, which they take only when asked; "@fp8qk" runs the
-# prefill tiles' score products on fp8 MFMAs, an opt-in arithmetic)
+# prefill tiles' score products on fp8 MFMAs and "@fp8" both of their products, opt-in arithmetic)
 DEFAULT_ALSO = ("mixed-8b@mfma", "decode-8b", "decode-8b@mfma", "long-context-8b", "prefill-fp8-64x8",
-                "prefill-fp8-64x8@fp8qk", "decode-fp8-64x8", "decode-fp8-64x8@valu")
-PATHS = {"": (0, 0), "valu": (1, 0), "mfma": (2, 0), "fp8qk": (0, 2)}   # suffix -> (row path, tile path)
-PATH_NOTES = {"": "", "valu": " (vector-ALU rows)", "mfma": " (MFMA rows)", "fp8qk": " (fp8 scores)"}
+                "prefill-fp8-64x8@fp8qk", "prefill-fp8-64x8@fp8", "decode-fp8-64x8", "decode-fp8-64x8@valu")
+PATHS = {"": (0, 0), "valu": (1, 0), "mfma": (2, 0), "fp8qk": (0, 2), "fp8": (0, 3)}   # suffix -> (rows, tiles)
+PATH_NOTES = {"": "", "valu": " (vector-ALU rows)", "mfma": " (MFMA rows)", "fp8qk": " (fp8 scores)",
+              "fp8": " (fp8 scores and values)"}
 
 
 def algorithmic_bytes(b) -> float:
@@ -673,17 +674,19 @@ def run_workload(name: str, args, log, full: bool = True, row_path: int = 0, til
     achieved_tfs = flops / (attn_ms * 1e-3) / 1e12
     # counters were taken with the planner's default paths only
     traffic = measured_traffic(b.name) if row_path == 0 and tile_path == 0 else None
-    # the matrix peak of the prefill work: bf16, or with fp8 score products
-    # half of the flops (Q K^T) at the fp8 peak and half (P V) at the bf16 one
-    mfma_peak = (MFMA_BF16_PEAK_TFS if tile_path != 2 else
-                 2.0 / (1.0 / MFMA_FP8_PEAK_TFS + 1.0 / MFMA_BF16_PEAK_TFS))
+    # the matrix peak of the prefill work: bf16; with fp8 score products half
+    # of the flops (Q K^T) at the fp8 peak and half (P V) at the bf16 one; with
+    # both products in fp8 the fp8 peak
+    mfma_peak = {2: 2.0 / (1.0 / MFMA_FP8_PEAK_TFS + 1.0 / MFMA_BF16_PEAK_TFS),
+                 3: MFMA_FP8_PEAK_TFS}.get(tile_path, MFMA_BF16_PEAK_TFS)
     # the batch is bound by whichever roof its algorithmic work reaches first
     if flops / (mfma_peak * 1e12) > nbytes / (HBM_PEAK_GBS * 1e9):
         roof = {"bound": "mfma", "achieved": round(achieved_tfs, 1), "peak": round(mfma_peak, 1),
                 "unit": "TFLOP/s", "frac": round(achieved_tfs / mfma_peak, 4),
                 "traffic": traffic, "hbm_gbs": round(achieved_gbs, 1)}
-        if tile_path == 2:
-            roof["peak_note"] = "Q K^T at the fp8 MFMA peak, P V at the bf16 one (half of the flops each)"
+        if tile_path in (2, 3):
+            roof["peak_note"] = ("Q K^T at the fp8 MFMA peak, P V at the bf16 one (half of the flops each)"
+                                 if tile_path == 2 else "both products at the fp8 MFMA peak")
             roof["frac_of_bf16_peak"] = round(achieved_tfs / MFMA_BF16_PEAK_TFS, 4)
     else:
         roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -713,7 +716,8 @@ def run_workload(name: str, args, log, full: bool = True, row_path: int = 0, til
                    "kv_heads": b.num_kv_heads, "head_dim": b.head_dim, "block_size": 16,
                    "kv_split_tokens": int(info.kv_split_tokens), "seed": args.seed, "pool_copies": n_copies,
                    "row_path": {1: "vector ALU", 2: "MFMA"}[int(info.row_path)],
-                   "tile_path": {1: "bf16", 2: "fp8 scores (opt-in)"}[int(info.tile_path)]},
+                   "tile_path": {1: "bf16", 2: "fp8 scores (opt-in)",
+                                 3: "fp8 scores and values (opt-in)"}[int(info.tile_path)]},
         "roofline": roof,
     }
     app_ms = np.array([a.elapsed_time(c) for a, c in ev_append])
@@ -748,8 +752,9 @@ def main():
                          "with its own roofline under 'workloads' (default for mixed-8b: " +
                          ",".join(DEFAULT_ALSO) + "; 'none' for no others)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--tile-path", choices=("auto", "fp8qk"), default="auto",
-                    help="fp8qk: the prefill tiles' score products on fp8 MFMAs (opt-in arithmetic)")
+    ap.add_argument("--tile-path", choices=("auto", "fp8qk", "fp8"), default="auto",
+                    help="fp8qk: the prefill tiles' score products on fp8 MFMAs; fp8: both of their products "
+                         "(opt-in arithmetic)")
     ap.add_argument("--row-path", choices=("auto", "valu", "mfma"), default="auto",
                     help="where the main workload's row items run: the planner's choice (MFMA for eight query "
                          "heads per KV head), the vector ALUs, or MFMA (eight or four heads per KV head)")
@@ -790,7 +795,7 @@ def main():
         return
     result = run_workload(args.workload, args, log, full=True,
                           row_path={"auto": 0, "valu": 1, "mfma": 2}[args.row_path],
-                          tile_path=2 if args.tile_path == "fp8qk" else 0)
+                          tile_path={"auto": 0, "fp8qk": 2, "fp8": 3}[args.tile_path])
     if args.also is None:
         also = list(DEFAULT_ALSO) if args.workload == "mixed-8b" else []
     else:

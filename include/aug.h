@@ -155,17 +155,24 @@ typedef struct {
  * only when asked for. */
 typedef enum { AUG_ROWS_AUTO = 0, AUG_ROWS_VALU = 1, AUG_ROWS_MFMA = 2 } aug_row_path;
 
-/* Arithmetic of the prefill tiles' score products S = Q K^T. BF16: Q and
- * the (converted) keys as bf16 on 32x32x16 MFMAs, the default. FP8_QK, for
- * fp8 KV with bf16 Q and head_dim 128 only: the keys stay fp8 and each query
- * vector (row and head) is rounded to E4M3 with its own scale (largest
- * magnitude / 448; a vector below 2^-100 becomes zero), on 32x32x64 fp8
- * MFMAs at twice the rate; P V stays bf16; decode rows are not affected. Rounding Q to 3
- * mantissa bits moves a logit by about 2^-5 of |q| |k| sqrt(head_dim) times
- * the softmax scale, so outputs stay within the bf16 tolerances for
- * near-uniform attention (keys of norm about 1) but not for sharp attention
- * (keys of norm about sqrt(head_dim)): opt-in, never chosen by AUTO. */
-typedef enum { AUG_TILES_AUTO = 0, AUG_TILES_BF16 = 1, AUG_TILES_FP8_QK = 2 } aug_tile_path;
+/* Arithmetic of the prefill tiles' products S = Q K^T and O = P V. BF16: Q,
+ * P and the (converted) keys and values as bf16 on 32x32x16 MFMAs, the
+ * default. FP8_QK, for fp8 KV with bf16 Q and head_dim 128 only: the keys
+ * stay fp8 and each query vector (row and head) is rounded to E4M3 with its
+ * own scale (largest magnitude / 448; a vector below 2^-100 becomes zero), on
+ * 32x32x64 fp8 MFMAs at twice the rate; P V stays bf16; decode rows are not
+ * affected. Rounding Q to 3 mantissa bits moves a logit by about 2^-5 of
+ * |q| |k| sqrt(head_dim) times the softmax scale, so outputs stay within the
+ * bf16 tolerances for near-uniform attention (keys of norm about 1) but not
+ * for sharp attention (keys of norm about sqrt(head_dim)). FP8 (same shapes):
+ * FP8_QK, and P V on 32x32x64 fp8 MFMAs as well: the values stay fp8 and each
+ * probability is rounded to E4M3 after scaling by its block's V scale over
+ * the item's largest one (the row sums add the rounded probabilities, so a
+ * single dominant key still returns its value); probabilities below 2^-15 of
+ * the row maximum vanish and the rest carry a relative error of up to 2^-4,
+ * which adds to the output error of FP8_QK where several keys share the
+ * weight. Both fp8 forms are opt-in, never chosen by AUTO. */
+typedef enum { AUG_TILES_AUTO = 0, AUG_TILES_BF16 = 1, AUG_TILES_FP8_QK = 2, AUG_TILES_FP8 = 3 } aug_tile_path;
 
 /* Planner options (aug_attn_plan_opts). */
 typedef struct {
@@ -198,7 +205,7 @@ aug_status aug_attn_plan(const aug_attn_shape* shape, const aug_batch_desc* batc
  * row items run on and the arithmetic of the prefill tiles (info->row_path
  * and info->tile_path record the resolved choices, which aug_attn_mixed
  * follows). Same image layout and errors, plus AUG_ERR_UNSUPPORTED for
- * AUG_ROWS_MFMA or AUG_TILES_FP8_QK on a shape without that path and
+ * AUG_ROWS_MFMA, AUG_TILES_FP8_QK or AUG_TILES_FP8 on a shape without that path and
  * AUG_ERR_INVALID for an unknown path or a non-zero reserved field. */
 aug_status aug_attn_plan_opts(const aug_attn_shape* shape, const aug_batch_desc* batch,
                               const aug_plan_options* opts, void* plan_host, size_t plan_cap,

@@ -32,7 +32,7 @@ AUG_F32, AUG_BF16, AUG_FP8_E4M3FN = 0, 1, 2
 AUG_WAITING, AUG_RUNNING, AUG_SWAPPED, AUG_PAUSED = 0, 1, 2, 3
 AUG_POL_NONE, AUG_PRESERVE, AUG_DISCARD, AUG_SWAP = 0, 1, 2, 3
 AUG_ROWS_AUTO, AUG_ROWS_VALU, AUG_ROWS_MFMA = 0, 1, 2
-AUG_TILES_AUTO, AUG_TILES_BF16, AUG_TILES_FP8_QK = 0, 1, 2
+AUG_TILES_AUTO, AUG_TILES_BF16, AUG_TILES_FP8_QK, AUG_TILES_FP8 = 0, 1, 2, 3
 
 DTYPE_CODES = {"f32": AUG_F32, "bf16": AUG_BF16, "fp8": AUG_FP8_E4M3FN}
 

@@ -849,6 +849,9 @@ template <int D>
 struct TileLds {
   static constexpr int KS = D + 8;    // K row stride (elements): 16-byte aligned, conflict-free reads
   static constexpr int KS8 = D + 16;  // K row stride (bytes) of fp8 keys kept as codes
+  // fp8 values kept as codes, transposed: one row of 64 key bytes per
+  // dimension (16 bytes of padding spread a 16-row read over all banks)
+  static constexpr int VT8 = 80;
   // V row stride (elements): rows 64 bytes apart modulo the 256-byte bank
   // width, so the transposing reads of four consecutive rows hit distinct banks
   static constexpr int VS = D + 32;
@@ -859,6 +862,7 @@ struct TileLds {
   static constexpr int NSC = 12;
   static constexpr int SCALES = 2 * NSC * 4;
   static constexpr int BYTES = 2 * STAGE + IDS * 4 + SCALES;
+  static_assert(D * VT8 <= 64 * VS * 2, "transposed fp8 values fit the V region of a stage");
 };
 
 // Staging of one thread's share of a key tile: 16-byte bf16 chunks, or
@@ -912,13 +916,26 @@ template <bool B> using bool_tag = std::integral_constant<bool, B>;
 // Tiles that every row reads in full (all keys at or below the first row's
 // position and inside the span, all block ids inside the pool) take a path
 // without per-key conditions; only the diagonal and span-end tiles mask.
-template <int KVT, int D, int G, int OT, bool QK8>
+//
+// F8 selects the arithmetic of the two products: 0 both bf16; 1 the score
+// products S = Q K^T on fp8 MFMAs (queries rounded to E4M3 per row); 2 also
+// P V on fp8 MFMAs (probabilities rounded to E4M3, values as stored).
+template <int KVT, int D, int G, int OT, int F8>
 __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* smem) {
   using L = TileLds<D>;
   using TS = TileStage<KVT>;
   using raw_t = typename TS::raw_t;
   constexpr bool FP8 = KVT == KV_FP8;
+  constexpr bool QK8 = F8 >= 1;
+  constexpr bool PV8 = F8 >= 2;
   static_assert(!QK8 || (FP8 && D == 128), "fp8 score products need fp8 keys and head_dim 128");
+  // fp8 probabilities: a lane's P values are stored as E4M3 codes of
+  // p * (vs_b / vref) * 2^kPv8Log2, with vs_b the block's V scale and vref the
+  // largest V scale of the item; p stays below 2^kSlack between rescales, so
+  // the codes stay below 2^(kSlack + kPv8Log2) = 256 (E4M3 reaches 448) and
+  // probabilities down to 2^-15 of the row maximum remain nonzero
+  constexpr float kSlack = PV8 ? 2.f : kRescaleSlack;
+  constexpr float kPv8Log2 = 6.f;
   constexpr int EB = FP8 ? 1 : 2;     // bytes per K/V element
   constexpr int KSTEPS = D / 16;      // k-steps of S^T over head_dim
   constexpr int DB = D / 32;          // 32-dim blocks of O^T
@@ -1008,6 +1025,11 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
 
   const int tc = threadIdx.x % CPR;
   const int tk = threadIdx.x / CPR;
+  // fp8 values are staged transposed; their loads put the key groups on
+  // neighbouring threads instead, so each wave's transposed LDS writes
+  // spread over the banks (the loads then take 32-byte pieces of 16 rows)
+  const int tkv = PV8 ? threadIdx.x % (64 / KPT) : tk;
+  const int tcv = PV8 ? threadIdx.x / (64 / KPT) : tc;
   const int key_end = it.key_end;
   const int t0 = it.key_begin / 64;
   const int t1 = (key_end + 63) / 64;
@@ -1022,22 +1044,61 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   const int blk_first = it.key_begin / kBlock;
   const int n_ids = (key_end + kBlock - 1) / kBlock - blk_first;
   int bad = 0;
+  float vmax = 0.f;   // fp8 probabilities: the item's largest V scale
   for (int i = threadIdx.x; i < n_ids && i < L::IDS; i += kThreads) {
     const int32_t id = a.block_ids[it.bt_off + blk_first + i];
     ids[i] = id;
-    bad |= static_cast<uint32_t>(id) >= static_cast<uint32_t>(a.num_pool_blocks);
+    const bool id_ok = static_cast<uint32_t>(id) < static_cast<uint32_t>(a.num_pool_blocks);
+    bad |= !id_ok;
+    if constexpr (PV8) {
+      if (id_ok) vmax = fmaxf(vmax, a.v_scale[static_cast<int64_t>(id) * a.hkv + kvh]);
+    }
+  }
+  if constexpr (PV8) {
+    // per-wave maxima into the second stage's scale slots, which are free
+    // until the first step's barrier
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) vmax = fmaxf(vmax, __shfl_xor(vmax, o));
+    if (lane == 0) stage_scales[L::NSC + wave] = vmax;
   }
   bad = __syncthreads_or(bad);
+  // exponent offset of the fp8 probabilities: log2(2^kPv8Log2 / vref) (a zero
+  // scale counts as 2^-100, as for the blocks)
+  float vbias = 0.f;
+  if constexpr (PV8) {
+    float vref = 0x1p-100f;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) vref = fmaxf(vref, stage_scales[L::NSC + w]);
+    vbias = kPv8Log2 - __builtin_amdgcn_logf(vref);
+  }
   const int t_full = bad ? t0 : max(t0, min(t1, min(it.pos0 + 1, key_end) / 64));
 
   // a thread stages KPT consecutive keys of one block (KPT divides 16)
   raw_t kr[KPT], vr[KPT];
   float sc_reg = 1.f;   // fp8: thread t < 8 carries scale t of the tile (k0..3, v0..3)
+  // KPT consecutive key rows (dims 8 tcx .. 8 tcx + 7) of `src`, zero where
+  // past the span or in a block outside the pool
+  auto load_rows = [&](const char* src, int k0, int tkx, int tcx, raw_t (&dst)[KPT], auto full_tag) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    const int tok0 = k0 + tkx * KPT;
+    const int slot = (tok0 >> 4) - blk_first;
+    const int bid = FULL || tok0 < key_end ? ids[slot] : -1;
+    const bool ok = FULL || static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
+    const int64_t base = ((static_cast<int64_t>(bid) * a.hkv + kvh) * head_stride +
+                          static_cast<int64_t>(tok0 & 15) * D + 8 * tcx) * EB;
+#pragma unroll
+    for (int u = 0; u < KPT; ++u)
+      dst[u] = FULL || (ok && tok0 + u < key_end) ? *reinterpret_cast<const raw_t*>(src + base + static_cast<int64_t>(u) * D * EB)
+                                                  : raw_t{};
+  };
   auto load_tile = [&](int k0, auto full_tag) {
     constexpr bool FULL = decltype(full_tag)::value;
     const int tok0 = k0 + tk * KPT;
     const int slot = (tok0 >> 4) - blk_first;
-    if constexpr (FULL) {
+    if constexpr (PV8) {
+      load_rows(kc, k0, tk, tc, kr, full_tag);
+      load_rows(vc, k0, tkv, tcv, vr, full_tag);
+    } else if constexpr (FULL) {
       const int64_t base = ((static_cast<int64_t>(ids[slot]) * a.hkv + kvh) * head_stride +
                             static_cast<int64_t>(tok0 & 15) * D + 8 * tc) * EB;
 #pragma unroll
@@ -1082,7 +1143,31 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       } else {
         *reinterpret_cast<uint4*>(ks + (tk * KPT + u) * L::KS + 8 * tc) = TS::to_bf16(kr[u]);
       }
-      *reinterpret_cast<uint4*>(vs + (tk * KPT + u) * L::VS + 8 * tc) = TS::to_bf16(vr[u]);
+      if constexpr (!PV8) *reinterpret_cast<uint4*>(vs + (tk * KPT + u) * L::VS + 8 * tc) = TS::to_bf16(vr[u]);
+    }
+    if constexpr (PV8) {
+      // V^T: the thread's four keys 4 tkv + t become byte t of one dword per
+      // dimension. In a row, key 32mb + 8j + 4h + t sits at byte
+      // 32h + 16mb + 4j + t, so a lane half's 32 keys of the score layout
+      // (those with bit 2 equal to h) are one contiguous 32-byte operand.
+      unsigned char* vt = reinterpret_cast<unsigned char*>(vs);
+      const int pos = 32 * (tkv & 1) + 16 * (tkv >> 3) + 4 * ((tkv & 7) >> 1);
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const uint32_t x0 = half ? vr[0].y : vr[0].x, x1 = half ? vr[1].y : vr[1].x;
+        const uint32_t x2 = half ? vr[2].y : vr[2].x, x3 = half ? vr[3].y : vr[3].x;
+        const uint32_t t01lo = __builtin_amdgcn_perm(x1, x0, 0x05010400u);   // keys 0, 1 of dims 0, 1
+        const uint32_t t01hi = __builtin_amdgcn_perm(x1, x0, 0x07030602u);   // keys 0, 1 of dims 2, 3
+        const uint32_t t23lo = __builtin_amdgcn_perm(x3, x2, 0x05010400u);
+        const uint32_t t23hi = __builtin_amdgcn_perm(x3, x2, 0x07030602u);
+        const uint32_t col[4] = {__builtin_amdgcn_perm(t23lo, t01lo, 0x05040100u),
+                                 __builtin_amdgcn_perm(t23lo, t01lo, 0x07060302u),
+                                 __builtin_amdgcn_perm(t23hi, t01hi, 0x05040100u),
+                                 __builtin_amdgcn_perm(t23hi, t01hi, 0x07060302u)};
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+          *reinterpret_cast<uint32_t*>(vt + (8 * tcv + 4 * half + d) * L::VT8 + pos) = col[d];
+      }
     }
     if constexpr (FP8) {
       // K: the score coefficient of the block; V: its scale enters each
@@ -1169,16 +1254,32 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     // lanes i/4, 4 + i/4, 8 + i/4 and 12 + i/4 of its group, so addressing
     // row (lane % 16) / 4 at column 4 (lane % 4) hands each lane four
     // consecutive keys of one dimension: the operand layout of V^T.
-    uint4 vop[4][DB];
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
+    uint4 vop[PV8 ? 1 : 4][PV8 ? 1 : DB];
+    // fp8 values: lane (dimension n of a 32-dim block, half hh) takes the 32
+    // codes of its dimension for the keys whose bit 2 is hh
+    v8i_t vop8[PV8 ? DB : 1];
+    if constexpr (PV8) {
+      const unsigned char* vt = reinterpret_cast<const unsigned char*>(vs);
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const uint16_t* v0 = vs + (16 * s) * L::VS + 32 * db + v_lane_off;
-        const uint2 lo = ds_read_tr16(v0);
-        const uint2 hi = ds_read_tr16(v0 + 8 * L::VS);
-        vop[s][db] = uint4{lo.x, lo.y, hi.x, hi.y};
+        const unsigned char* src = vt + (32 * db + n) * L::VT8 + 32 * hh;
+        const uint4 lo = *reinterpret_cast<const uint4*>(src);
+        const uint4 hi = *reinterpret_cast<const uint4*>(src + 16);
+        vop8[db] = v8i_t{static_cast<int>(lo.x), static_cast<int>(lo.y), static_cast<int>(lo.z),
+                         static_cast<int>(lo.w), static_cast<int>(hi.x), static_cast<int>(hi.y),
+                         static_cast<int>(hi.z), static_cast<int>(hi.w)};
       }
+    } else {
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const uint16_t* v0 = vs + (16 * s) * L::VS + 32 * db + v_lane_off;
+          const uint2 lo = ds_read_tr16(v0);
+          const uint2 hi = ds_read_tr16(v0 + 8 * L::VS);
+          vop[s][db] = uint4{lo.x, lo.y, hi.x, hi.y};
+        }
+    }
 
     // Entry (mb, i, j) of this lane is key k0 + 32mb + 8i + 4hh + j, which
     // lies in block b = 2mb + i/2 of the tile; b is also the PV step that
@@ -1215,7 +1316,7 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     if constexpr (!FP8) smax *= c;
     smax = max_across_halves(smax);
     const float mn = fmaxf(m_run, smax);
-    if (__any(mn > m_run + kRescaleSlack)) {
+    if (__any(mn > m_run + kSlack)) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - mn);
       l_run *= alpha;
 #pragma unroll
@@ -1230,6 +1331,39 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     // packed values (fp8: weighted back by 1/vs)
     // O^T += V^T P^T, 16 keys (one block) per step; k-slots of lane half hh
     // are keys {16s+4hh+j, 16s+8+4hh+j}, exactly the S^T entries this lane holds
+    if constexpr (PV8) {
+      // O^T += V^T P^T for all 64 keys at once, one 32x32x64 fp8 MFMA per
+      // 32-dim block. Codes p * (vs_b / vref) * 2^kPv8Log2: dword 2s + i of
+      // the operand holds block s's entries 4i .. 4i + 3 of this lane, the
+      // byte order of the V^T rows. The row sum adds the rounded codes
+      // (exact in bf16) weighed back by 1/vs_b.
+      v8i_t pop8;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const int mb = s >> 1, e0 = 8 * (s & 1);
+        const float bias = vlog[s] + vbias - m_run;
+        float pv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = __builtin_amdgcn_exp2f(fmaf(sacc[mb][e0 + e], coef[s], bias));
+          pv[e] = live(mb, e0 + e) ? x : 0.f;
+        }
+        int w0 = __builtin_amdgcn_cvt_pk_fp8_f32(pv[0], pv[1], 0, false);
+        w0 = __builtin_amdgcn_cvt_pk_fp8_f32(pv[2], pv[3], w0, true);
+        int w1 = __builtin_amdgcn_cvt_pk_fp8_f32(pv[4], pv[5], 0, false);
+        w1 = __builtin_amdgcn_cvt_pk_fp8_f32(pv[6], pv[7], w1, true);
+        pop8[2 * s] = w0;
+        pop8[2 * s + 1] = w1;
+        const float bsum = dot2_bf16(fp8x2_to_bf16x2<true>(w1), kBf16PairOne,
+                           dot2_bf16(fp8x2_to_bf16x2<false>(w1), kBf16PairOne,
+                           dot2_bf16(fp8x2_to_bf16x2<true>(w0), kBf16PairOne,
+                           dot2_bf16(fp8x2_to_bf16x2<false>(w0), kBf16PairOne, 0.f))));
+        l_run = fmaf(bsum, vinv[s], l_run);
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        acc_o[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop8[db], pop8, acc_o[db], 0, 0, 0, 127, 0, 127);
+    } else {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       const int mb = s >> 1, e0 = 8 * (s & 1);
@@ -1252,6 +1386,7 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
 #pragma unroll
       for (int db = 0; db < DB; ++db)
         acc_o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vop[s][db]), pop, acc_o[db], 0, 0, 0);
+    }
     }
     // From here to the next tile's score MFMAs (barrier, staging of the tile
     // after next, reads of the K operands) this wave issues ahead of the
@@ -1307,7 +1442,9 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
             float4{acc_o[db][4 * i], acc_o[db][4 * i + 1], acc_o[db][4 * i + 2], acc_o[db][4 * i + 3]};
       }
     if (hh == 0) {
-      pp[G * D + gh] = m_run;
+      // fp8 probabilities carry the item's factor 2^vbias in both the
+      // outputs and the row sum: it enters the partial's maximum
+      pp[G * D + gh] = PV8 ? m_run - vbias : m_run;
       pp[G * D + G + gh] = l_tot;
     }
   }
@@ -1327,7 +1464,7 @@ constexpr bool row_mfma_capable() {
   return (G == 8 || G == 4) && D == 128 && (KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16;
 }
 
-template <int KVT, int D, int G, int QT, int OT, bool TILES, bool ROW_MFMA, int NW, bool QK8 = false>
+template <int KVT, int D, int G, int QT, int OT, bool TILES, bool ROW_MFMA, int NW, int F8 = 0>
 __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   static_assert(!TILES || NW == kThreads / 64, "tile items run on four-wave workgroups");
   constexpr int RB = row_lds_bytes<D, G, NW>();
@@ -1337,7 +1474,7 @@ __device__ __forceinline__ void attn_body(const AttnArgs& a) {
   const WorkItem it = a.items[blockIdx.x];
   if constexpr (TILES) {
     if (it.kind == aug::kTileItem) {
-      tile_item<KVT, D, G, OT, QK8>(it, a, smem);
+      tile_item<KVT, D, G, OT, F8>(it, a, smem);
       return;
     }
   }
@@ -1358,9 +1495,9 @@ __global__ __launch_bounds__(64 * NW) void attn_rows_kernel(AttnArgs a) {
 // Mixed batches: MFMA tiles and row items in one launch. The tile path's
 // accumulators set the register budget (two waves per SIMD); the row path
 // spends the same budget on prefetching the next block.
-template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA, bool QK8>
+template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA, int F8>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_mixed_kernel(AttnArgs a) {
-  attn_body<KVT, D, G, QT, OT, true, ROW_MFMA, kThreads / 64, QK8>(a);
+  attn_body<KVT, D, G, QT, OT, true, ROW_MFMA, kThreads / 64, F8>(a);
 }
 
 // Merge launch for split prefill tiles: one workgroup per (row, KV head)
@@ -1428,15 +1565,19 @@ template <int KVT, int D, int G, int QT, int OT, bool ROW_MFMA>
 aug_status launch_rows(const AttnArgs& a, const aug_attn_plan_info& info, hipStream_t st) {
   if (info.num_prefill_items > 0) {
     if constexpr ((KVT == KV_BF16 || KVT == KV_FP8) && QT == AUG_BF16) {
-      if (info.tile_path == AUG_TILES_FP8_QK) {
+      if (info.tile_path == AUG_TILES_FP8_QK || info.tile_path == AUG_TILES_FP8) {
         if constexpr (KVT == KV_FP8 && D == 128) {
-          hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA, true>), dim3(info.num_items),
-                             dim3(kThreads), 0, st, a);
+          if (info.tile_path == AUG_TILES_FP8)
+            hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA, 2>), dim3(info.num_items),
+                               dim3(kThreads), 0, st, a);
+          else
+            hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA, 1>), dim3(info.num_items),
+                               dim3(kThreads), 0, st, a);
         } else {
-          return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: fp8 score products need fp8 KV and head_dim 128");
+          return aug::fail(AUG_ERR_UNSUPPORTED, "aug_attn_mixed: fp8 tile products need fp8 KV and head_dim 128");
         }
       } else {
-        hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA, false>), dim3(info.num_items),
+        hipLaunchKernelGGL((attn_mixed_kernel<KVT, D, G, QT, OT, ROW_MFMA, 0>), dim3(info.num_items),
                            dim3(kThreads), 0, st, a);
       }
     } else {

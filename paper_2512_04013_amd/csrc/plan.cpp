@@ -89,7 +89,8 @@ aug_status check_plan_info(const aug_attn_plan_info* info, const aug_attn_shape*
                 s->out_dtype);
   if (info->row_path != AUG_ROWS_VALU && !(info->row_path == AUG_ROWS_MFMA && row_mfma_supported(*s)))
     return fail(AUG_ERR_INVALID, "%s: info names row path %d, which this shape cannot run", who, info->row_path);
-  if (info->tile_path != AUG_TILES_BF16 && !(info->tile_path == AUG_TILES_FP8_QK && tile_fp8qk_supported(*s)))
+  if (info->tile_path != AUG_TILES_BF16 &&
+      !((info->tile_path == AUG_TILES_FP8_QK || info->tile_path == AUG_TILES_FP8) && tile_fp8qk_supported(*s)))
     return fail(AUG_ERR_INVALID, "%s: info names tile path %d, which this shape cannot run", who,
                 info->tile_path);
   return AUG_OK;
@@ -172,11 +173,12 @@ extern "C" aug_status aug_attn_plan_opts(const aug_attn_shape* s, const aug_batc
   if (row_path == AUG_ROWS_AUTO)
     row_path = row_mfma_supported(*s) && s->num_q_heads == 8 * s->num_kv_heads ? AUG_ROWS_MFMA : AUG_ROWS_VALU;
   int32_t tile_path = opts->tile_path;
-  if (tile_path != AUG_TILES_AUTO && tile_path != AUG_TILES_BF16 && tile_path != AUG_TILES_FP8_QK)
+  if (tile_path != AUG_TILES_AUTO && tile_path != AUG_TILES_BF16 && tile_path != AUG_TILES_FP8_QK &&
+      tile_path != AUG_TILES_FP8)
     return fail(AUG_ERR_INVALID, "%s: unknown tile path %d", who, tile_path);
-  if (tile_path == AUG_TILES_FP8_QK && !tile_fp8qk_supported(*s))
-    return fail(AUG_ERR_UNSUPPORTED, "%s: fp8 score products need fp8 KV, bf16 queries and head_dim 128", who);
-  if (tile_path == AUG_TILES_AUTO) tile_path = AUG_TILES_BF16;   // fp8 scores are opt-in
+  if ((tile_path == AUG_TILES_FP8_QK || tile_path == AUG_TILES_FP8) && !tile_fp8qk_supported(*s))
+    return fail(AUG_ERR_UNSUPPORTED, "%s: fp8 tile products need fp8 KV, bf16 queries and head_dim 128", who);
+  if (tile_path == AUG_TILES_AUTO) tile_path = AUG_TILES_BF16;   // fp8 tile products are opt-in
   if (!b || !info) return fail(AUG_ERR_INVALID, "%s: batch or info is NULL", who);
   const int32_t n = b->num_reqs;
   if (n < 0) return fail(AUG_ERR_INVALID, "%s: num_reqs %d < 0", who, n);

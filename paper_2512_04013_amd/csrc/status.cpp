@@ -32,4 +32,4 @@ extern "C" const char* aug_status_string(aug_status s) {
 
 extern "C" const char* aug_last_error(void) { return g_last_error; }
 
-extern "C" int32_t aug_abi_version(void) { return (3 << 16) | 0; }
+extern "C" int32_t aug_abi_version(void) { return (3 << 16) | 1; }

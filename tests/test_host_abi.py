@@ -374,10 +374,11 @@ def test_default_split_doubles_for_mfma_rows_without_tiles():
 
 
 def test_tile_path_option_resolves_and_is_checked():
-    """fp8 score products on the tiles are opt-in: AUTO resolves to bf16; FP8_QK
-    is accepted for fp8 KV with bf16 queries (head_dim 128) and refused for
-    other dtype sets; the resolved path is in the info and the plan header,
-    and a call refuses an info naming a path its shape lacks."""
+    """fp8 products on the tiles are opt-in: AUTO resolves to bf16; FP8_QK
+    (scores) and FP8 (scores and values) are accepted for fp8 KV with bf16
+    queries (head_dim 128) and refused for other dtype sets; the resolved
+    path is in the info and the plan header, and a call refuses an info
+    naming a path its shape lacks."""
     L = aug.lib()
     q_start, ctx = [0, 5, 6], [50, 20]
     bt_start = np.concatenate([[0], np.cumsum([-(-c // 16) for c in ctx])])
@@ -386,20 +387,26 @@ def test_tile_path_option_resolves_and_is_checked():
     b16 = aug.make_shape(16, 2, 128, "bf16", "bf16", "bf16", 0.088)
     info, plan = aug.aug_attn_plan(f8, q_start, ctx, bt_start, pool)
     assert info.tile_path == aug.AUG_TILES_BF16 and plan[62] == aug.AUG_TILES_BF16
-    info, plan = aug.aug_attn_plan(f8, q_start, ctx, bt_start, pool, tile_path=aug.AUG_TILES_FP8_QK)
-    assert info.tile_path == aug.AUG_TILES_FP8_QK and plan[62] == aug.AUG_TILES_FP8_QK
+    for tp in (aug.AUG_TILES_FP8_QK, aug.AUG_TILES_FP8):
+        info, plan = aug.aug_attn_plan(f8, q_start, ctx, bt_start, pool, tile_path=tp)
+        assert info.tile_path == tp and plan[62] == tp
     info16, _ = aug.aug_attn_plan(b16, q_start, ctx, bt_start, pool, tile_path=aug.AUG_TILES_BF16)
     assert info16.tile_path == aug.AUG_TILES_BF16
-    with pytest.raises(AugError) as e:
-        aug.aug_attn_plan(b16, q_start, ctx, bt_start, pool, tile_path=aug.AUG_TILES_FP8_QK)
-    assert e.value.status == aug.AUG_ERR_UNSUPPORTED
+    f8_d64 = aug.make_shape(16, 2, 64, "bf16", "fp8", "bf16", 0.125)
+    for shape in (b16, f8_d64):
+        for tp in (aug.AUG_TILES_FP8_QK, aug.AUG_TILES_FP8):
+            with pytest.raises(AugError) as e:
+                aug.aug_attn_plan(shape, q_start, ctx, bt_start, pool, tile_path=tp)
+            assert e.value.status == aug.AUG_ERR_UNSUPPORTED
     with pytest.raises(AugError) as e:
         aug.aug_attn_plan(f8, q_start, ctx, bt_start, pool, tile_path=9)
     assert e.value.status == aug.AUG_ERR_INVALID
-    bad = aug.aug_attn_plan_info.from_buffer_copy(info16)
-    bad.tile_path = aug.AUG_TILES_FP8_QK
-    st = L.aug_attn_mixed(aug.C.byref(b16), aug.C.byref(bad), 8, 8, 8, 8, None, None, 8, pool, 8, 8, 1 << 40, None)
-    assert st == aug.AUG_ERR_INVALID and "tile path" in aug.aug_last_error()
+    for tp in (aug.AUG_TILES_FP8_QK, aug.AUG_TILES_FP8, 4):
+        bad = aug.aug_attn_plan_info.from_buffer_copy(info16)
+        bad.tile_path = tp
+        st = L.aug_attn_mixed(aug.C.byref(b16), aug.C.byref(bad), 8, 8, 8, 8, None, None, 8, pool, 8, 8, 1 << 40,
+                              None)
+        assert st == aug.AUG_ERR_INVALID and "tile path" in aug.aug_last_error()
 
 
 def test_noalloc_attention_rejects_bad_arguments_without_touching_the_gpu():
