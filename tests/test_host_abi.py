@@ -352,9 +352,9 @@ def test_row_path_option_resolves_and_is_checked():
 def test_default_split_doubles_for_mfma_rows_without_tiles():
     """A launch of MFMA row items alone runs eight-wave workgroups and takes
     decode spans twice as long as four-wave row items: 1024 instead of 512
-    keys on a small batch, 8192 instead of 4096 on a large one. Row items
-    beside prefill tiles, and VALU row items, keep the four-wave spans; an
-    explicit split is taken as given."""
+    keys on a small batch, 8192 on a large one. Four-wave row items keep 512
+    on a small batch and go up to 6144 keys in a launch of their own, 4096
+    beside prefill tiles; an explicit split is taken as given."""
     def plan(shape, q_len, ctx, **kw):
         q_start = np.concatenate([[0], np.cumsum(q_len)])
         bt_start = np.concatenate([[0], np.cumsum([-(-c // 16) for c in ctx])])
@@ -366,7 +366,9 @@ def test_default_split_doubles_for_mfma_rows_without_tiles():
     assert plan(g8, [1] * 20, small, row_path=aug.AUG_ROWS_VALU).kv_split_tokens == 512
     assert plan(g8, [1] * 19 + [64], small).kv_split_tokens == 512      # one prefill chunk: tiles
     assert plan(g8, [1] * 512, large).kv_split_tokens == 8192
-    assert plan(g8, [1] * 512, large, row_path=aug.AUG_ROWS_VALU).kv_split_tokens == 4096
+    assert plan(g8, [1] * 512, large, row_path=aug.AUG_ROWS_VALU).kv_split_tokens == 6144
+    assert plan(g8, [1] * 511 + [64], large).kv_split_tokens == 4096              # beside tiles
+    assert plan(g8, [1] * 511 + [64], large, row_path=aug.AUG_ROWS_VALU).kv_split_tokens == 4096
     assert plan(g8, [1] * 20, small, kv_split_tokens=300).kv_split_tokens == 304
     g4 = aug.make_shape(32, 8, 128, "bf16", "bf16", "bf16", 0.088)
     assert plan(g4, [1] * 20, small).kv_split_tokens == 512
