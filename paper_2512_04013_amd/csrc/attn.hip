@@ -1064,21 +1064,28 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
   bad = __syncthreads_or(bad);
   // exponent offset of the fp8 probabilities: log2(2^kPv8Log2 / vref) (a zero
   // scale counts as 2^-100, as for the blocks)
-  float vbias = 0.f;
+  float vbias = 0.f, vref = 1.f, vsmall = 0.f;
   if constexpr (PV8) {
-    float vref = 0x1p-100f;
+    vref = 0x1p-100f;
 #pragma unroll
     for (int w = 0; w < kThreads / 64; ++w) vref = fmaxf(vref, stage_scales[L::NSC + w]);
     vbias = kPv8Log2 - __builtin_amdgcn_logf(vref);
+    // A block whose V scale is below 2^-8 of vref (an all-zero block has
+    // scale 0) would round its probability codes to zero or nearly, and its
+    // keys would drop out of the row sum. Such a block is staged with zero
+    // values and vref's own scale terms instead: its keys keep their weight,
+    // and its values, at most 2^-8 of the item's largest, are left out.
+    vsmall = vref * 0x1p-8f;
   }
   const int t_full = bad ? t0 : max(t0, min(t1, min(it.pos0 + 1, key_end) / 64));
 
   // a thread stages KPT consecutive keys of one block (KPT divides 16)
   raw_t kr[KPT], vr[KPT];
   float sc_reg = 1.f;   // fp8: thread t < 8 carries scale t of the tile (k0..3, v0..3)
+  float vsc_reg = 1.f;  // fp8 values: the V scale of the block this thread stages
   // KPT consecutive key rows (dims 8 tcx .. 8 tcx + 7) of `src`, zero where
   // past the span or in a block outside the pool
-  auto load_rows = [&](const char* src, int k0, int tkx, int tcx, raw_t (&dst)[KPT], auto full_tag) {
+  auto load_rows = [&](const char* src, int k0, int tkx, int tcx, raw_t (&dst)[KPT], auto full_tag) -> int {
     constexpr bool FULL = decltype(full_tag)::value;
     const int tok0 = k0 + tkx * KPT;
     const int slot = (tok0 >> 4) - blk_first;
@@ -1090,6 +1097,7 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     for (int u = 0; u < KPT; ++u)
       dst[u] = FULL || (ok && tok0 + u < key_end) ? *reinterpret_cast<const raw_t*>(src + base + static_cast<int64_t>(u) * D * EB)
                                                   : raw_t{};
+    return ok ? bid : -1;
   };
   auto load_tile = [&](int k0, auto full_tag) {
     constexpr bool FULL = decltype(full_tag)::value;
@@ -1097,7 +1105,8 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
     const int slot = (tok0 >> 4) - blk_first;
     if constexpr (PV8) {
       load_rows(kc, k0, tk, tc, kr, full_tag);
-      load_rows(vc, k0, tkv, tcv, vr, full_tag);
+      const int vbid = load_rows(vc, k0, tkv, tcv, vr, full_tag);
+      vsc_reg = vbid >= 0 ? a.v_scale[static_cast<int64_t>(vbid) * a.hkv + kvh] : 1.f;
     } else if constexpr (FULL) {
       const int64_t base = ((static_cast<int64_t>(ids[slot]) * a.hkv + kvh) * head_stride +
                             static_cast<int64_t>(tok0 & 15) * D + 8 * tc) * EB;
@@ -1152,10 +1161,11 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       // (those with bit 2 equal to h) are one contiguous 32-byte operand.
       unsigned char* vt = reinterpret_cast<unsigned char*>(vs);
       const int pos = 32 * (tkv & 1) + 16 * (tkv >> 3) + 4 * ((tkv & 7) >> 1);
+      const uint32_t keep = fmaxf(vsc_reg, 0x1p-100f) < vsmall ? 0u : 0xFFFFFFFFu;
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
-        const uint32_t x0 = half ? vr[0].y : vr[0].x, x1 = half ? vr[1].y : vr[1].x;
-        const uint32_t x2 = half ? vr[2].y : vr[2].x, x3 = half ? vr[3].y : vr[3].x;
+        const uint32_t x0 = (half ? vr[0].y : vr[0].x) & keep, x1 = (half ? vr[1].y : vr[1].x) & keep;
+        const uint32_t x2 = (half ? vr[2].y : vr[2].x) & keep, x3 = (half ? vr[3].y : vr[3].x) & keep;
         const uint32_t t01lo = __builtin_amdgcn_perm(x1, x0, 0x05010400u);   // keys 0, 1 of dims 0, 1
         const uint32_t t01hi = __builtin_amdgcn_perm(x1, x0, 0x07030602u);   // keys 0, 1 of dims 2, 3
         const uint32_t t23lo = __builtin_amdgcn_perm(x3, x2, 0x05010400u);
@@ -1178,7 +1188,8 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       if (threadIdx.x < 4) {
         ss[threadIdx.x] = c * sc_reg;
       } else if (threadIdx.x < 8) {
-        const float v = fmaxf(sc_reg, 0x1p-100f);
+        float v = fmaxf(sc_reg, 0x1p-100f);
+        if constexpr (PV8) v = v < vsmall ? vref : v;   // staged as zeros (see vsmall)
         ss[threadIdx.x] = __builtin_amdgcn_logf(v);
         ss[threadIdx.x + 4] = __builtin_amdgcn_rcpf(v);
       }

@@ -272,3 +272,28 @@ def test_fp8_values_relaunch_repeats_the_bits():
         out = att.run(q, kv=kv, block_ids=bids)
         torch.cuda.synchronize()
         assert np.array_equal(rt.to_host_f64(out), first)
+
+
+def test_fp8_values_blocks_of_zero_values_keep_their_weight():
+    """Blocks whose values are all zero (V scale 0) or far smaller than the
+    item's largest scale round their probability codes to zero; their keys
+    must still count in the softmax denominator. Every third block of each
+    chunk's context is zeroed (codes and scale) and one more is scaled down
+    2^-12: outputs within the plain-input law of the exact oracle (without
+    the mass of those keys the outputs would grow by about half)."""
+    q_lens, ctx_lens = [100, 40, 1], [1700, 900, 600]
+    b = make_batch_from_lengths("fp8pv-zero-v", q_lens, ctx_lens, num_q_heads=64, num_kv_heads=8, head_dim=128,
+                                q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16", n_pool_blocks=256, seed=51,
+                                kv_std=1.0 / np.sqrt(128))
+    v = b.v_cache.copy()
+    vs = b.v_scale.copy()
+    for r in range(2):
+        table = b.block_ids[b.bt_start[r]:b.bt_start[r + 1]]
+        zero = table[::3]
+        v[zero] = 0
+        vs[zero] = 0.0
+        vs[table[1]] *= 2.0 ** -12
+    b.v_cache, b.v_scale = v, vs
+    got, _ = _run(b, tile_path=FP8)
+    chunk = _rows(b, False)
+    _check_law(got[chunk], oa.attention_for(b)[chunk], PV_PLAIN_LAW, "zero and tiny value blocks vs exact oracle")
