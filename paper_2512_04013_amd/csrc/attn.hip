@@ -116,6 +116,12 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// OCP E4M3FN byte pair (bytes 0-1, or 2-3 with HI) -> exact bf16 pair
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+}
+
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
@@ -478,11 +484,16 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
     }
     const bool bid_ok = static_cast<uint32_t>(bid) < static_cast<uint32_t>(a.num_pool_blocks);
     const int tok0 = blk * kBlock;
-    float ksc = sc, vsc = 1.f;
+    float ksc = sc, vsc = 1.f, vlog = 0.f, vinv = 1.f;
     if constexpr (KVT == KV_FP8) {
       if (bid_ok) {
         ksc = sc * a.k_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
         vsc = a.v_scale[static_cast<int64_t>(bid) * a.hkv + kvh];
+        // bf16 probabilities carry the V scale through its log2 and the row
+        // sum weighs it back (a zero scale is taken as 2^-100)
+        const float vs = fmaxf(vsc, 0x1p-100f);
+        vlog = __builtin_amdgcn_logf(vs);
+        vinv = __builtin_amdgcn_rcpf(vs);
       }
     }
     // a block is either entirely inside the span (no masking at all) or the
@@ -527,17 +538,61 @@ __device__ void row_item(const WorkItem& it, const AttnArgs& a, float* lds) {
         m[h] = mn[h];
       }
     }
+    if constexpr (KVT == KV_F32) {
 #pragma unroll
-    for (int i = 0; i < NLD; ++i) {
-      float vf[VEC];
-      F::to_f32(vraw[i], vf);
+      for (int i = 0; i < NLD; ++i) {
+        float vf[VEC];
+        F::to_f32(vraw[i], vf);
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float p = __builtin_amdgcn_exp2f(s[i][h] - m[h]);
-        l[h] += p;
-        const float pv = p * vsc;
+        for (int h = 0; h < G; ++h) {
+          const float p = __builtin_amdgcn_exp2f(s[i][h] - m[h]);
+          l[h] += p;
+          const float pv = p * vsc;
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) o[h][e] = fmaf(pv, vf[e], o[h][e]);
+          for (int e = 0; e < VEC; ++e) o[h][e] = fmaf(pv, vf[e], o[h][e]);
+        }
+      }
+    } else {
+      // The lane's tokens go in pairs (loads i and i + 1 of the block): their
+      // probabilities are packed to one bf16 pair, the values of each dim to
+      // another, and one packed dot product adds both tokens' terms. The row
+      // sum adds exactly the packed probabilities, as the MFMA paths do.
+      static_assert(NLD % 2 == 0 && VEC == 8, "row tokens pair up, eight dims per lane");
+#pragma unroll
+      for (int i = 0; i < NLD; i += 2) {
+        uint32_t vp[VEC];   // dim e of tokens i and i + 1, as one bf16 pair
+        if constexpr (KVT == KV_BF16) {
+          const uint32_t a0[4] = {vraw[i].x, vraw[i].y, vraw[i].z, vraw[i].w};
+          const uint32_t a1[4] = {vraw[i + 1].x, vraw[i + 1].y, vraw[i + 1].z, vraw[i + 1].w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            vp[2 * k] = __builtin_amdgcn_perm(a1[k], a0[k], 0x05040100u);
+            vp[2 * k + 1] = __builtin_amdgcn_perm(a1[k], a0[k], 0x07060302u);
+          }
+        } else {
+          // fp8: interleave the two tokens' codes, then convert each byte
+          // pair exactly to a bf16 pair
+#pragma unroll
+          for (int k = 0; k < 2; ++k) {
+            const uint32_t x0 = k ? vraw[i].y : vraw[i].x, x1 = k ? vraw[i + 1].y : vraw[i + 1].x;
+            const uint32_t lo = __builtin_amdgcn_perm(x1, x0, 0x05010400u);   // dims 4k, 4k+1
+            const uint32_t hi = __builtin_amdgcn_perm(x1, x0, 0x07030602u);   // dims 4k+2, 4k+3
+            vp[4 * k + 0] = fp8x2_to_bf16x2<false>(lo);
+            vp[4 * k + 1] = fp8x2_to_bf16x2<true>(lo);
+            vp[4 * k + 2] = fp8x2_to_bf16x2<false>(hi);
+            vp[4 * k + 3] = fp8x2_to_bf16x2<true>(hi);
+          }
+        }
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float bias = vlog - m[h];
+          const uint32_t pp = pack_bf16(__builtin_amdgcn_exp2f(s[i][h] + bias),
+                                        __builtin_amdgcn_exp2f(s[i + 1][h] + bias));
+          const float psum = dot2_bf16(pp, kBf16PairOne, 0.f);
+          l[h] = KVT == KV_FP8 ? fmaf(psum, vinv, l[h]) : l[h] + psum;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) o[h][e] = dot2_bf16(pp, vp[e], o[h][e]);
+        }
       }
     }
   }
@@ -617,11 +672,6 @@ __device__ __forceinline__ float group4_sum(float v) {
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 
-// OCP E4M3FN byte pair (bytes 0-1, or 2-3 with HI) -> exact bf16 pair
-template <bool HI>
-__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w) {
-  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
-}
 
 template <int KVT> struct MfmaRowKv;
 template <> struct MfmaRowKv<KV_BF16> {

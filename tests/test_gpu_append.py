@@ -84,7 +84,7 @@ def test_append_is_bit_exact_and_attention_reads_it(case):
         compare(got, want, qd, what=f"attention after append, case {case}")
         return
     # New rows far larger than the configured N(0,1) inputs. A departure from
-    # the stated gate, on purpose: the MFMA paths round each probability to
+    # the stated gate, on purpose: the bf16 and fp8 paths round each probability to
     # bf16 (relative 2^-9) before the P.V product, which moves an output by at
     # most 2^-9 * max|v - o| / (1 - 2^-9) <= 2^-8 * max|v|, plus half an ulp
     # of the bf16 output; the fixed 1e-2 gate therefore holds only while
