@@ -40,12 +40,13 @@ CASES = [
 ]
 
 
-def _run(batch, kv_split=0, tile_path=FP8_QK):
+def _run(batch, kv_split=0, tile_path=FP8_QK, row_path=0):
     from paper_2512_04013_amd import runtime as rt
     shape, kv, q, bids = rt.upload_batch(batch, staging_bytes=1 << 26)
     att = rt.MixedAttention(shape, kv, batch.q_start, batch.ctx_len, batch.bt_start, batch.block_ids,
-                            bids, kv_split_tokens=kv_split, tile_path=tile_path)
+                            bids, kv_split_tokens=kv_split, tile_path=tile_path, row_path=row_path)
     assert att.info.tile_path == tile_path
+    assert row_path == 0 or att.info.row_path == row_path
     out = att.run(q)
     torch.cuda.synchronize()
     return rt.to_host_f64(out), att
@@ -297,3 +298,35 @@ def test_fp8_values_blocks_of_zero_values_keep_their_weight():
     got, _ = _run(b, tile_path=FP8)
     chunk = _rows(b, False)
     _check_law(got[chunk], oa.attention_for(b)[chunk], PV_PLAIN_LAW, "zero and tiny value blocks vs exact oracle")
+
+
+@pytest.mark.parametrize("tile_path", [FP8_QK, FP8])
+@pytest.mark.parametrize("sharp", [False, True])
+def test_fp8_tiles_beside_four_head_mfma_rows(tile_path, sharp):
+    """Four-head groups on the opt-in MFMA rows next to the opt-in fp8 tile
+    products, in one launch (an instantiation of its own): decode rows at the
+    bf16 gate against the exact oracle, chunk rows against both oracles
+    within the tile path's law, with and without split decode rows."""
+    q_lens, ctx_lens, hq, hkv = CASES[2]
+    assert hq == 4 * hkv
+    b = make_batch_from_lengths(f"fp8-mfma4-{tile_path}", q_lens, ctx_lens, num_q_heads=hq, num_kv_heads=hkv,
+                                head_dim=128, q_dtype="bf16", kv_dtype="fp8", out_dtype="bf16",
+                                n_pool_blocks=1024, seed=310, kv_std=1.0 if sharp else 1.0 / np.sqrt(128))
+    say(f"[fp8 tiles + MFMA rows] G=4 tile_path={tile_path} sharp={sharp}")
+    want_rounded = oa.attention_for(b, fp8_chunk_queries=True)
+    want_exact = oa.attention_for(b)
+    chunk, dec = _rows(b, False), _rows(b, True)
+    for split in (0, 48):
+        got, att = _run(b, kv_split=split, tile_path=tile_path, row_path=2)
+        what = f"G=4 MFMA rows, tile path {tile_path}, sharp={sharp}, split={split}"
+        compare(got, want_exact, "bf16", rows=dec, what=what + " decode rows")
+        if tile_path == FP8:
+            law = PV_SHARP_LAW if sharp else PV_PLAIN_LAW
+            _check_law(got[chunk], want_rounded[chunk], law, what + " chunk rows vs rounded-Q oracle")
+            _check_law(got[chunk], want_exact[chunk], law, what + " chunk rows vs exact oracle")
+        else:
+            compare(got, want_rounded, "bf16", rows=chunk, what=what + " chunk rows vs rounded-Q oracle")
+            if sharp:
+                _check_law(got[chunk], want_exact[chunk], SHARP_LAW, what + " chunk rows vs exact oracle")
+            else:
+                compare(got, want_exact, "bf16", rows=chunk, what=what + " chunk rows vs exact oracle")
