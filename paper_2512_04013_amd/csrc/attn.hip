@@ -1364,17 +1364,29 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       vinv[b] = FP8 ? stage_scales[stage * L::NSC + 8 + b] : 1.f;
     }
     // row maximum of the scaled scores: block maxima of the raw scores times
-    // the (non-negative) block coefficients
-    float smax = -INFINITY;
+    // the (non-negative) block coefficients. The raw scores are finite or
+    // -inf (masked), so the NaN-propagating maximum (three operands per
+    // instruction, no canonicalising of its inputs) gives the same value;
+    // fp8 blocks combine with fmaxf, which drops the NaN of a masked block
+    // under a zero key scale.
+    float smax;
+    if constexpr (FP8) {
+      smax = -INFINITY;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int mb = b >> 1, e0 = 8 * (b & 1);
-      float bm = sacc[mb][e0];
+      for (int b = 0; b < 4; ++b) {
+        const int mb = b >> 1, e0 = 8 * (b & 1);
+        float bm = sacc[mb][e0];
 #pragma unroll
-      for (int e = 1; e < 8; ++e) bm = fmaxf(bm, sacc[mb][e0 + e]);
-      smax = fmaxf(smax, FP8 ? bm * coef[b] : bm);
+        for (int e = 1; e < 8; ++e) bm = __builtin_elementwise_maximum(bm, sacc[mb][e0 + e]);
+        smax = fmaxf(smax, bm * coef[b]);
+      }
+    } else {
+      // one coefficient for the whole tile: one chain over its 32 entries
+      smax = sacc[0][0];
+#pragma unroll
+      for (int e = 1; e < 32; ++e) smax = __builtin_elementwise_maximum(smax, sacc[e >> 4][e & 15]);
+      smax *= c;
     }
-    if constexpr (!FP8) smax *= c;
     smax = max_across_halves(smax);
     const float mn = fmaxf(m_run, smax);
     if (__any(mn > m_run + kSlack)) {
@@ -1440,9 +1452,11 @@ __device__ void tile_item(const WorkItem& it, const AttnArgs& a, unsigned char* 
       pw.y = pack_bf16(pv[2], pv[3]);
       pw.z = pack_bf16(pv[4], pv[5]);
       pw.w = pack_bf16(pv[6], pv[7]);
+      // bf16 KV adds the packed probabilities straight into the row sum;
+      // fp8 weighs the block's sum by 1/vs first
       const float bsum = dot2_bf16(pw.w, kBf16PairOne, dot2_bf16(pw.z, kBf16PairOne,
-                         dot2_bf16(pw.y, kBf16PairOne, dot2_bf16(pw.x, kBf16PairOne, 0.f))));
-      l_run = FP8 ? fmaf(bsum, vinv[s], l_run) : l_run + bsum;
+                         dot2_bf16(pw.y, kBf16PairOne, dot2_bf16(pw.x, kBf16PairOne, FP8 ? 0.f : l_run))));
+      l_run = FP8 ? fmaf(bsum, vinv[s], l_run) : bsum;
       const bf16x8_t pop = as_bf16x8(pw);
 #pragma unroll
       for (int db = 0; db < DB; ++db)
