@@ -107,11 +107,24 @@ def append_bytes(b, info) -> float:
     return n + items * (16 + 4)
 
 
-def measured_traffic(workload_name: str):
+def traffic_key(workload_name: str, row_path: int = 0, tile_path: int = 0):
+    """Name of a workload's counter record: the workload itself on the
+    planner's default paths, ``<workload>@<suffix>`` on an opt-in path (the
+    suffixes of PATHS)."""
+    for suffix, paths in PATHS.items():
+        if paths == (row_path, tile_path):
+            return workload_name + ("@" + suffix if suffix else "")
+    return None
+
+
+def measured_traffic(workload_name):
     """HBM bytes per attention call from the committed rocprofv3 counter
-    summary, or None when the summary does not cover this workload or the
-    kernel and planner sources have changed since the counters were taken."""
+    summary, or None when the summary does not cover this workload (or path)
+    or the kernel and planner sources have changed since the counters were
+    taken."""
     import hashlib
+    if workload_name is None:
+        return None
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     if not os.path.exists(path):
         return None
@@ -672,8 +685,7 @@ def run_workload(name: str, args, log, full: bool = True, row_path: int = 0, til
     flops = prefill_flops(b)
     achieved_gbs = nbytes / (attn_ms * 1e-3) / 1e9
     achieved_tfs = flops / (attn_ms * 1e-3) / 1e12
-    # counters were taken with the planner's default paths only
-    traffic = measured_traffic(b.name) if row_path == 0 and tile_path == 0 else None
+    traffic = measured_traffic(traffic_key(b.name, row_path, tile_path))
     # the matrix peak of the prefill work: bf16; with fp8 score products half
     # of the flops (Q K^T) at the fp8 peak and half (P V) at the bf16 one; with
     # both products in fp8 the fp8 peak
